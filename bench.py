@@ -1,0 +1,563 @@
+#!/usr/bin/env python3
+"""KV-cache streaming benchmark on one MI355X.
+
+A step is one pass of the streaming hot path over the OPT-13B pipeline-stage
+workload (10 of 40 layers, 40 heads x 128, batch 8, capacity 2048, fp16,
+prompt lengths uniform 512..1024 from the seed):
+
+  prompt stream-out (dense pack) -> prompt stream-in into a second cache
+  (dense unpack) -> 128 decode-step increments, each packed out of the
+  sender and streamed into the receiver.
+
+Inputs are resident in HBM before timing starts.  ``value`` is algorithmic
+bytes per step (every payload byte read once and written once: 2 x payload
+per call) over the step time, in GB/s.  ``roofline`` is the bulk pack kernel
+(the dense-run kernel of the prompt stream-out) timed with HIP events on its
+stream.  Further objects report the other kernels, the microbatch swap over
+the host link (OPT-66B stage), the paged gather/scatter (LLaMA-2-70B GQA),
+the full-cache replica and restore (BLOOM-176B shard), and the oracle timed
+on the host cores.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extras]
+                       [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+PCIE_PEAK_GBS = 63.0        # PCIe Gen5 x16 per direction after 128b/130b encoding
+METRIC = "KV pack/scatter GB/s and % of HBM peak; swap GB/s vs host-link peak (1 GPU)"
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--no-extras", action="store_true")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--graph", action="store_true",
+                   help="replay each step as one captured HIP graph")
+    return p.parse_args()
+
+
+class Timer:
+    """HIP-event pairs on one stream; mean duration in ms."""
+
+    def __init__(self, torch, stream):
+        self.torch, self.stream, self.pairs = torch, stream, []
+
+    def __enter__(self):
+        a = self.torch.cuda.Event(enable_timing=True)
+        a.record(self.stream)
+        self.pairs.append([a, None])
+        return self
+
+    def __exit__(self, *exc):
+        b = self.torch.cuda.Event(enable_timing=True)
+        b.record(self.stream)
+        self.pairs[-1][1] = b
+
+    def mean_ms(self) -> float:
+        ts = [a.elapsed_time(b) for a, b in self.pairs]
+        return sum(ts) / len(ts)
+
+    def min_ms(self) -> float:
+        return min(a.elapsed_time(b) for a, b in self.pairs)
+
+
+def flush_l2(torch, scratch):
+    """Overwrite 512 MB so no payload is served from L2 / MALL."""
+    scratch.add_(1)
+
+
+def main_step_bench(args, torch, dv, synth):
+    dev = torch.device("cuda:0")
+    w = synth.make_workload(1)
+    L, H, D, B, S = w.layers, w.heads, w.head_dim, w.batch, w.max_seq
+    nbytes = w.dense_bytes()
+    stream = torch.cuda.current_stream()
+    sender = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    synth.device_fill(sender.data_ptr(), nbytes, w.data_seed, stream=stream.cuda_stream)
+    recv = torch.zeros(nbytes, dtype=torch.uint8, device=dev)
+    cs = dv.Cache(dv.DV_DENSE, L, H, D, B, [sender], max_seq=S)
+    cr = dv.Cache(dv.DV_DENSE, L, H, D, B, [recv], max_seq=S)
+    t0, t1 = w.prompt_ranges()
+    P = dv.dv_packed_bytes(cs, 0, L, t0, t1)
+    wire = torch.empty(P, dtype=torch.uint8, device=dev)
+    pos = [w.step_positions(i) for i in range(w.steps)]
+    I = dv.dv_packed_bytes(cs, 0, L, pos[0], pos[0] + 1)
+    incs = torch.empty(I, dtype=torch.uint8, device=dev)
+    ends = [p + 1 for p in pos]
+
+    t_pack = Timer(torch, stream)
+    t_unpack = Timer(torch, stream)
+    t_tok = Timer(torch, stream)
+    t_tokin = Timer(torch, stream)
+
+    def step(timed: bool):
+        if timed:
+            with t_pack:
+                dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, P, stream)
+            with t_unpack:
+                dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, stream)
+        else:
+            dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, P, stream)
+            dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, stream)
+        for i in range(w.steps):
+            if timed and i == 0:
+                with t_tok:
+                    dv.dv_stream_out_token(cs, 0, 0, L, pos[i], incs, I, stream)
+                with t_tokin:
+                    dv.dv_stream_in(cr, 0, 0, L, pos[i], ends[i], incs, I, stream)
+            else:
+                dv.dv_stream_out_token(cs, 0, 0, L, pos[i], incs, I, stream)
+                dv.dv_stream_in(cr, 0, 0, L, pos[i], ends[i], incs, I, stream)
+
+    graph = None
+    if args.graph:
+        s = torch.cuda.Stream()
+        s.wait_stream(stream)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(s):
+            step(False)  # warm
+            with torch.cuda.graph(graph, stream=s):
+                gs = torch.cuda.current_stream()
+                dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, P, gs)
+                dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, gs)
+                for i in range(w.steps):
+                    dv.dv_stream_out_token(cs, 0, 0, L, pos[i], incs, I, gs)
+                    dv.dv_stream_in(cr, 0, 0, L, pos[i], ends[i], incs, I, gs)
+        torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        if graph is not None:
+            graph.replay()
+        else:
+            step(False)
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(args.steps):
+        if graph is not None:
+            graph.replay()
+        else:
+            step(True)
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / args.steps
+    log(f"timed {args.steps} steps: {ms:.3f} ms/step")
+    step_bytes = 2 * P * 2 + w.steps * 2 * I * 2
+    res = {
+        "ms": ms, "P": P, "I": I, "step_bytes": step_bytes,
+        "value": step_bytes / (ms * 1e-3) / 1e9,
+    }
+    if graph is None:
+        res["pack_ms"] = t_pack.mean_ms()
+        res["unpack_ms"] = t_unpack.mean_ms()
+        res["tok_ms"] = t_tok.mean_ms()
+        res["tokin_ms"] = t_tokin.mean_ms()
+    else:
+        # time the bulk kernels separately for the roofline
+        for _ in range(3):
+            with t_pack:
+                dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, P, stream)
+            with t_unpack:
+                dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, stream)
+        torch.cuda.synchronize()
+        res["pack_ms"] = t_pack.mean_ms()
+        res["unpack_ms"] = t_unpack.mean_ms()
+    del sender, recv, wire, incs
+    torch.cuda.empty_cache()
+    return w, res
+
+
+def increments_bench(torch, dv, synth):
+    """Per-call latency of decode-step increments (eager and graph-replayed)."""
+    dev = torch.device("cuda:0")
+    out = {}
+    for idx in (1, 2, 4):
+        w = synth.make_workload(idx)
+        L, H, D, B = w.layers, w.heads, w.head_dim, w.batch
+        stream = torch.cuda.current_stream()
+        if w.paged:
+            nbytes = w.pool_bytes()
+            buf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+            bt = torch.from_numpy(w.block_table_a).to(dev)
+            c = dv.Cache(dv.DV_PAGED, L, H, D, B, [buf], block_size=w.block_size,
+                         num_blocks=w.num_blocks, max_blocks=w.max_blocks, block_tables=[bt])
+        else:
+            nbytes = w.dense_bytes()
+            buf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+            c = dv.Cache(dv.DV_DENSE, L, H, D, B, [buf], max_seq=S_of(w))
+        synth.device_fill(buf.data_ptr(), nbytes, w.data_seed, stream=stream.cuda_stream)
+        p = w.step_positions(0)
+        I = dv.dv_packed_bytes(c, 0, L, p, p + 1)
+        inc = torch.empty(I, dtype=torch.uint8, device=dev)
+        n = 200
+        for _ in range(10):
+            dv.dv_stream_out_token(c, 0, 0, L, p, inc, I, stream)
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n):
+            dv.dv_stream_out_token(c, 0, 0, L, p, inc, I, stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        eager_us = a.elapsed_time(b) / n * 1e3
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(stream)
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                for _ in range(n):
+                    dv.dv_stream_out_token(c, 0, 0, L, p, inc, I, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        a.record(stream)
+        g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        graph_us = a.elapsed_time(b) / n * 1e3
+        out[w.name] = {
+            "bytes": I, "eager_us_per_call": round(eager_us, 3),
+            "graph_us_per_call": round(graph_us, 3),
+            "eager_GBps_2x": round(2 * I / (eager_us * 1e-6) / 1e9, 1),
+            "graph_GBps_2x": round(2 * I / (graph_us * 1e-6) / 1e9, 1),
+            "hbm_roofline_us": round(2 * I / (HBM_PEAK_GBS * 1e9) * 1e6, 3),
+        }
+        del buf, inc, g
+        torch.cuda.empty_cache()
+    return out
+
+
+def S_of(w):
+    return w.max_seq
+
+
+def bulk_bench(torch, dv, synth, idx, reps=10):
+    """Bulk stream-out and stream-in of one workload, timed per call."""
+    dev = torch.device("cuda:0")
+    w = synth.make_workload(idx)
+    L, H, D, B = w.layers, w.heads, w.head_dim, w.batch
+    stream = torch.cuda.current_stream()
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    if w.paged:
+        nbytes = w.pool_bytes()
+        a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        r = torch.zeros(nbytes, dtype=torch.uint8, device=dev)
+        bta = torch.from_numpy(w.block_table_a).to(dev)
+        btb = torch.from_numpy(w.block_table_b).to(dev)
+        ca = dv.Cache(dv.DV_PAGED, L, H, D, B, [a], block_size=w.block_size,
+                      num_blocks=w.num_blocks, max_blocks=w.max_blocks, block_tables=[bta])
+        cr = dv.Cache(dv.DV_PAGED, L, H, D, B, [r], block_size=w.block_size,
+                      num_blocks=w.num_blocks, max_blocks=w.max_blocks, block_tables=[btb])
+    else:
+        nbytes = w.dense_bytes()
+        a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        r = torch.zeros(nbytes, dtype=torch.uint8, device=dev)
+        ca = dv.Cache(dv.DV_DENSE, L, H, D, B, [a], max_seq=w.max_seq)
+        cr = dv.Cache(dv.DV_DENSE, L, H, D, B, [r], max_seq=w.max_seq)
+    synth.device_fill(a.data_ptr(), nbytes, w.data_seed, stream=stream.cuda_stream)
+    t0, t1 = w.prompt_ranges()
+    P = dv.dv_packed_bytes(ca, 0, L, t0, t1)
+    wire = torch.empty(P, dtype=torch.uint8, device=dev)
+    tp, tu = Timer(torch, stream), Timer(torch, stream)
+    for i in range(reps + 2):
+        flush_l2(torch, scratch)
+        if i >= 2:
+            with tp:
+                dv.dv_stream_out_prompt(ca, 0, 0, L, t0, t1, wire, P, stream)
+        else:
+            dv.dv_stream_out_prompt(ca, 0, 0, L, t0, t1, wire, P, stream)
+        flush_l2(torch, scratch)
+        if i >= 2:
+            with tu:
+                dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, stream)
+        else:
+            dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, stream)
+    torch.cuda.synchronize()
+    res = {"payload_bytes": P}
+    for name, t in (("stream_out", tp), ("stream_in", tu)):
+        ms = t.mean_ms()
+        gbs = 2 * P / (ms * 1e-3) / 1e9
+        res[name] = {"ms": round(ms, 4), "GBps_2x": round(gbs, 1),
+                     "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
+    del a, r, wire, scratch
+    torch.cuda.empty_cache()
+    return w, res
+
+
+def swap_bench(torch, dv, synth, reps=3):
+    """OPT-66B stage microbatch swap over the host link (one slot, valid prefix)."""
+    dev = torch.device("cuda:0")
+    w = synth.make_workload(2)
+    L, H, D, B, S = w.layers, w.heads, w.head_dim, w.batch, w.max_seq
+    S_host = 1024
+    nb_dev = w.dense_bytes()
+    nb_host = w.dense_bytes(S_host)
+    slots = [torch.empty(nb_dev, dtype=torch.uint8, device=dev) for _ in range(2)]
+    for i, s in enumerate(slots):
+        synth.device_fill(s.data_ptr(), nb_dev, w.data_seed + i)
+    hosts = [torch.empty(nb_host, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
+    for h in hosts:
+        h.fill_(0)
+    ds = dv.Cache(dv.DV_DENSE, L, H, D, B, slots, max_seq=S)
+    hh = dv.Cache(dv.DV_DENSE, L, H, D, B, [h.data_ptr() for h in hosts], max_seq=S_host,
+                  mem=dv.DV_MEM_HOST_PINNED)
+    zero = np.zeros(B, np.int32)
+    lens = w.lens.astype(np.int32)
+    P = dv.dv_packed_bytes(ds, 0, L, zero, lens)
+    s_out, s_in = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    res = {"payload_bytes": P, "rows": 2 * L * B * H, "row_bytes": int(lens[0]) * D * 2,
+           "device_pitch": S * D * 2, "host_pitch": S_host * D * 2}
+    # swap-out alone, swap-in alone, then both directions at once
+    to, ti = Timer(torch, s_out), Timer(torch, s_in)
+    for _ in range(reps):
+        with to:
+            dv.dv_swap_out(ds, 0, hh, 0, 0, L, zero, lens, s_out)
+        s_out.synchronize()
+    for _ in range(reps):
+        with ti:
+            dv.dv_swap_in(hh, 1, ds, 1, 0, L, zero, lens, s_in)
+        s_in.synchronize()
+    out_ms, in_ms = to.mean_ms(), ti.mean_ms()
+    res["swap_out"] = {"ms": round(out_ms, 3), "GBps": round(P / (out_ms * 1e-3) / 1e9, 2)}
+    res["swap_in"] = {"ms": round(in_ms, 3), "GBps": round(P / (in_ms * 1e-3) / 1e9, 2)}
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(s_out)
+    s_in.wait_event(a)
+    dv.dv_swap_out(ds, 0, hh, 0, 0, L, zero, lens, s_out)
+    dv.dv_swap_in(hh, 1, ds, 1, 0, L, zero, lens, s_in)
+    s_out.wait_stream(s_in)
+    b.record(s_out)
+    torch.cuda.synchronize()
+    bi_ms = a.elapsed_time(b)
+    res["bidirectional"] = {"ms": round(bi_ms, 3),
+                            "GBps_total": round(2 * P / (bi_ms * 1e-3) / 1e9, 2)}
+    del t_start
+    # host-link calibration: one contiguous copy of the same byte count
+    flat_d = slots[0][:P]
+    flat_h = hosts[0][:P]
+    tc_o, tc_i = Timer(torch, s_out), Timer(torch, s_in)
+    for _ in range(reps):
+        with tc_o:
+            with torch.cuda.stream(s_out):
+                flat_h.copy_(flat_d, non_blocking=True)
+        s_out.synchronize()
+        with tc_i:
+            with torch.cuda.stream(s_in):
+                flat_d.copy_(flat_h, non_blocking=True)
+        s_in.synchronize()
+    res["calibration_contiguous"] = {
+        "d2h_GBps": round(P / (tc_o.mean_ms() * 1e-3) / 1e9, 2),
+        "h2d_GBps": round(P / (tc_i.mean_ms() * 1e-3) / 1e9, 2)}
+    link = read_link()
+    res["link"] = link
+    res["peak_GBps"] = PCIE_PEAK_GBS
+    res["frac_link"] = round(min(res["swap_out"]["GBps"], res["swap_in"]["GBps"]) /
+                             PCIE_PEAK_GBS, 4)
+    del slots, hosts
+    torch.cuda.empty_cache()
+    return res
+
+
+def read_link():
+    """PCIe link speed/width of the GPU from sysfs (best effort)."""
+    import glob
+    out = {}
+    for d in glob.glob("/sys/class/drm/card*/device"):
+        try:
+            vendor = open(os.path.join(d, "vendor")).read().strip()
+            if vendor != "0x1002":
+                continue
+            for k in ("current_link_speed", "current_link_width", "max_link_speed",
+                      "max_link_width"):
+                p = os.path.join(d, k)
+                if os.path.exists(p):
+                    out[k] = open(p).read().strip()
+            if out:
+                break
+        except OSError:
+            continue
+    return out or None
+
+
+def copy_calibration(torch, nbytes=4 << 30):
+    """Device-to-device copy of a known size: torch copy kernel and DMA."""
+    dev = torch.device("cuda:0")
+    a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    b = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    a.fill_(1)
+    stream = torch.cuda.current_stream()
+    t = Timer(torch, stream)
+    for i in range(6):
+        if i >= 2:
+            with t:
+                b.copy_(a)
+        else:
+            b.copy_(a)
+    torch.cuda.synchronize()
+    ms = t.mean_ms()
+    del a, b
+    torch.cuda.empty_cache()
+    return {"bytes": nbytes, "ms": round(ms, 4), "GBps_2x": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}
+
+
+def cpu_baseline():
+    """The oracle on the host cores: prompt stream-out and stream-in of the
+    OPT-13B stage (all 10 layers, 1.26 GB payload), no increments."""
+    import oracle
+    import synth
+
+    w = synth.make_workload(1)
+    lay = oracle.Layout(oracle.DENSE, w.layers, w.heads, w.head_dim, w.batch,
+                        seq_cap=w.max_seq, elem_bytes=2)
+    orc = oracle.get()
+    cache = synth.fill_bytes(lay.storage_bytes(), w.data_seed)
+    recv = np.zeros_like(cache)
+    recv[::4096] = 0  # touch the pages before timing
+    t0, t1 = w.prompt_ranges()
+    n = orc.wire_elems(lay, 0, w.layers, t0, t1) * 2
+    wire = np.empty(n, np.uint8)
+    wire[::4096] = 0
+    a = time.perf_counter()
+    import ctypes
+    p0 = np.ascontiguousarray(t0, np.int32)
+    p1 = np.ascontiguousarray(t1, np.int32)
+    rc = orc.lib.dvo_pack(ctypes.byref(lay._c), cache.ctypes.data, 0, w.layers, p0.ctypes.data,
+                          p1.ctypes.data, wire.ctypes.data)
+    b = time.perf_counter()
+    rc |= orc.lib.dvo_unpack(ctypes.byref(lay._c), recv.ctypes.data, 0, w.layers,
+                             p0.ctypes.data, p1.ctypes.data, wire.ctypes.data)
+    c = time.perf_counter()
+    assert rc == 0
+    secs = c - a
+    return {
+        "value": round(2 * 2 * n / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+        "sample": (f"prompt stream-out + stream-in of the OPT-13B stage, all {w.layers} "
+                   f"layers, {n} B payload, no increments; single-threaded C oracle "
+                   f"({b - a:.2f} s out, {c - b:.2f} s in)"),
+        "host_cpu": cpu_model(),
+        "affinity_cores": len(os.sched_getaffinity(0)),
+    }
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+import numpy as np  # noqa: E402
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only: the streaming path has no cross-GPU step "
+              f"here (asked for --gpus {args.gpus}, WORLD_SIZE {world})", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import synth
+    from paper_2403_01876_amd import dv
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    log(f"device: {torch.cuda.get_device_name(0)}")
+    w, r = main_step_bench(args, torch, dv, synth)
+    pack_gbs = 2 * r["P"] / (r["pack_ms"] * 1e-3) / 1e9
+    unpack_gbs = 2 * r["P"] / (r["unpack_ms"] * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(r["value"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["ms"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u16",
+        "data": "synthetic",
+        "config": {
+            "workload": ("opt13b-stage: 10 layers x 40 heads x 128 dims, batch 8, capacity "
+                         "2048, fp16 dense [layer][K|V][batch][head][seq][dim], prompts "
+                         "U[512,1024] from seed 1; step = prompt stream-out + stream-in + "
+                         "128 x (increment out + in)"),
+            "payload_prompt_bytes": r["P"],
+            "payload_increment_bytes": r["I"],
+            "algorithmic_bytes_per_step": r["step_bytes"],
+            "graph": bool(args.graph),
+        },
+        "roofline": {
+            "kernel": "dense_runs_kernel<pack> (prompt stream-out)",
+            "bound": "hbm",
+            "achieved": round(pack_gbs, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(pack_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "avg_ms": round(r["pack_ms"], 4),
+            "bytes_per_launch": 2 * r["P"],
+        },
+        "kernels": {
+            "dense_runs_kernel<unpack>": {"avg_ms": round(r["unpack_ms"], 4),
+                                          "GBps_2x": round(unpack_gbs, 1),
+                                          "frac_hbm": round(unpack_gbs / HBM_PEAK_GBS, 4)},
+        },
+    }
+    if "tok_ms" in r:
+        for k, key in (("token_kernel<pack>", "tok_ms"), ("token_kernel<unpack>", "tokin_ms")):
+            out["kernels"][k] = {"avg_ms_first_step": round(r[key], 4),
+                                 "GBps_2x": round(2 * r["I"] / (r[key] * 1e-3) / 1e9, 1)}
+    if not args.no_extras:
+        log("extras: increments")
+        out["increments"] = increments_bench(torch, dv, synth)
+        log("extras: bulk workloads")
+        for idx in (3, 4):
+            wk, res = bulk_bench(torch, dv, synth, idx)
+            out.setdefault("bulk", {})[wk.name] = res
+        log("extras: swap")
+        out["swap"] = swap_bench(torch, dv, synth)
+        log("extras: copy calibration")
+        out["calibration_d2d_copy"] = copy_calibration(torch)
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        out["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

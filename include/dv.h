@@ -1,0 +1,188 @@
+/* dv.h -- KV-cache streaming for one MI355X (gfx950): pack, unpack and swap.
+ *
+ * The operations are the data-movement core of the KV-cache streaming
+ * library of "DejaVu: KV-cache Streaming for Fast, Fault-tolerant Generative
+ * LLM Serving" (arXiv 2403.01876):
+ *
+ *   dv_stream_out_prompt  non-contiguous cache region -> one contiguous
+ *                         buffer (the "scatter" primitive of Table 1, with
+ *                         the buffered-copy optimisation of Sec. 4.1.1);
+ *   dv_stream_out_token   the one-token increment of every layer after a
+ *                         decode step (Sec. 4.1.1, Figure "cache_ft": each
+ *                         step updates a small non-contiguous part);
+ *   dv_stream_in          contiguous buffer -> a receiver's layout (the
+ *                         "gather" primitive of Table 1; repopulating a lost
+ *                         cache from its replica, Sec. 4.2.3);
+ *   dv_swap_out/_in       microbatch swapping between a GPU slot and pinned
+ *                         host memory (Sec. 4.2.2).
+ *
+ * Conventions shared by every call:
+ *  - Return value: DV_OK (0) or a negative dv_status.  Arguments are checked
+ *    on the host before anything is enqueued; on any error nothing is
+ *    enqueued and no memory is touched.
+ *  - Asynchrony: work is enqueued on `stream` (a hipStream_t; NULL is the
+ *    null stream) and is complete only once that stream has been
+ *    synchronised.  Host arrays passed in (ranges, mb_base, block_table) are
+ *    read during the call only and may be reused as soon as it returns.
+ *  - Ownership: the caller owns every buffer (caches, contiguous buffers,
+ *    block tables, host mirrors).  The library allocates nothing, keeps no
+ *    state between calls and frees nothing.
+ *  - Elements are opaque `elem_bytes`-byte words: results are bit copies
+ *    (NaN payloads, -0 and subnormals preserved).
+ *  - Aliasing: the source and destination of one call must not overlap
+ *    (checked; DV_ERR_INVALID).
+ *  - Thread safety: calls may be made from several host threads; calls on
+ *    different streams that write the same bytes race, as any two kernels
+ *    would.
+ */
+#ifndef DV_H
+#define DV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DV_API_VERSION 1
+
+typedef enum {
+  DV_OK = 0,
+  DV_ERR_INVALID = -1,     /* malformed descriptor or argument: null pointer, extent <= 0,
+                              head_dim*elem_bytes not a multiple of 16, base not 16-byte
+                              aligned, overlapping source and destination */
+  DV_ERR_RANGE = -2,       /* microbatch/slot index, layer range or token range outside the
+                              descriptor */
+  DV_ERR_SPACE = -3,       /* destination capacity (or source size) below the stream size */
+  DV_ERR_UNSUPPORTED = -4, /* well-formed but not handled (swap of a paged or split-key cache) */
+  DV_ERR_HIP = -5          /* the HIP runtime refused to enqueue the work */
+} dv_status;
+
+typedef enum {
+  DV_DENSE = 0,        /* [layer][K|V][batch][head][max_seq][head_dim] */
+  DV_PAGED = 1,        /* pool [layer][K|V][num_blocks][head][block_size][head_dim], tokens
+                          reach blocks through a per-sequence block table */
+  DV_DENSE_KSPLIT = 2  /* as DV_DENSE, except the key half stores head_dim in 16-byte groups
+                          outside the token axis: [layer][K][batch][head][head_dim/x][max_seq][x],
+                          x = 16/elem_bytes (the split-key layout of decoder kernels that
+                          read keys 16 bytes at a time); the value half is dense */
+} dv_kind;
+
+typedef enum { DV_MEM_DEVICE = 0, DV_MEM_HOST_PINNED = 1 } dv_mem;
+
+/* A KV-cache layout and where its microbatches live.  A cache holds one
+ * pipeline stage's layers and one tensor-parallel shard's heads, so
+ * num_layers and num_heads are local counts.  Logical element
+ * X(l, kv, b, h, s, d) -- layer l, kv 0 = key / 1 = value, sequence b, head
+ * h, token s, dimension d -- is stored at element index
+ *   DV_DENSE  ((((l*2+kv)*batch + b)*num_heads + h)*max_seq + s)*head_dim + d
+ *   DV_PAGED  ((((l*2+kv)*num_blocks + T[b][s/block_size])*num_heads + h)*block_size
+ *              + s%block_size)*head_dim + d,      T = block_table[mb]
+ *   DV_DENSE_KSPLIT, kv = 0:
+ *             (((((l*2)*batch + b)*num_heads + h)*(head_dim/x) + d/x)*max_seq + s)*x + d%x
+ * of microbatch mb's base address mb_base[mb].  All bases 16-byte aligned. */
+typedef struct dv_cache {
+  int32_t kind;        /* dv_kind */
+  int32_t mem;         /* dv_mem: where the cache bytes live (swap direction checks) */
+  int32_t elem_bytes;  /* bytes per element (2 for fp16/bf16) */
+  int32_t num_layers;  /* layers held */
+  int32_t num_heads;   /* KV heads held */
+  int32_t head_dim;    /* head_dim * elem_bytes must be a multiple of 16 */
+  int32_t batch;       /* sequences per microbatch */
+  int32_t max_seq;     /* dense kinds: token capacity per sequence; paged: ignored
+                          (capacity is max_blocks * block_size) */
+  int32_t block_size;  /* paged: tokens per block */
+  int32_t num_blocks;  /* paged: blocks in each microbatch's pool */
+  int32_t max_blocks;  /* paged: columns of each block table */
+  int32_t num_mb;      /* entries of mb_base (and block_table) */
+  void* const* mb_base;              /* host array [num_mb] of cache base addresses */
+  const int32_t* const* block_table; /* paged: host array [num_mb] of device addresses of
+                                        int32 [batch][max_blocks] tables; an entry outside
+                                        [0, num_blocks) marks an unmapped block */
+} dv_cache;
+
+/* The contiguous buffer ("wire") a stream produces or consumes, for layer
+ * range [l0, l1) and per-sequence token ranges [t0[b], t1[b]):
+ *   n_b = t1[b] - t0[b],  P_b = sum_{b' < b} n_b',  N = sum_b n_b,
+ *   X(l,kv,b,h,s,d) sits at element
+ *   ((l-l0)*2 + kv)*N*H*D + P_b*H*D + h*n_b*D + (s - t0[b])*D + d,
+ * i.e. [layer][K|V][sequence][head][token][head_dim] with ragged sequences,
+ * (l1-l0)*2*H*D*N*elem_bytes bytes in all.  It is headerless: the receiver
+ * passes the same ranges.  Layer ranges concatenate: the buffer of [l0, l1)
+ * is that of [l0, m) followed by that of [m, l1), so a prompt can be
+ * streamed layer by layer as each layer is computed (Sec. 4.1.1,
+ * optimisation 2). */
+
+/* Storage bytes of one microbatch of `c` (dense: L*2*B*H*S*D*E; paged:
+ * L*2*NB*H*bs*D*E).  Host-only.  DV_OK, DV_ERR_INVALID. */
+int dv_cache_bytes(const dv_cache* c, uint64_t* out_bytes);
+
+/* Bytes of the contiguous buffer for these ranges (formula above).  t0 may
+ * be NULL (all zero).  Host-only.  DV_OK, DV_ERR_INVALID, DV_ERR_RANGE. */
+int dv_packed_bytes(const dv_cache* c, int32_t l0, int32_t l1, const int32_t* t0,
+                    const int32_t* t1, uint64_t* out_bytes);
+
+/* Pack microbatch `mb` of `src`, layers [l0, l1), tokens [t0[b], t1[b]) of
+ * each sequence b, into `dst` in the wire order above.  A prompt stream
+ * passes t0 = NULL (or zeros) and t1 = prompt lengths; a whole-cache replica
+ * passes the valid lengths; an empty range (t0[b] == t1[b]) skips a
+ * sequence (e.g. a request that stopped early).  `dst` is device memory (or
+ * any memory kernels may write) of `dst_cap` bytes, 16-byte aligned.  On
+ * return *out_bytes (if not NULL) holds the stream size, also on
+ * DV_ERR_SPACE.  Paged caches: tokens whose table entry is outside
+ * [0, num_blocks) are rejected by no host check (the table is on the
+ * device); the kernel skips them and their wire bytes are left unwritten.
+ * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_HIP. */
+int dv_stream_out_prompt(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
+                         const int32_t* t0, const int32_t* t1, void* dst, uint64_t dst_cap,
+                         uint64_t* out_bytes, void* stream);
+
+/* Pack the decode-step increment: token pos[b] of every sequence, layers
+ * [l0, l1); pos[b] < 0 marks an inactive sequence (contributes nothing).
+ * Identical to dv_stream_out_prompt with t0 = pos, t1 = pos + 1 (0 tokens
+ * for inactive sequences), so the wire is [layer][K|V][active seq][head][D].
+ * Same arguments, errors and ownership as dv_stream_out_prompt. */
+int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
+                        const int32_t* pos, void* dst, uint64_t dst_cap, uint64_t* out_bytes,
+                        void* stream);
+
+/* Unpack `src` (a wire of exactly dv_packed_bytes bytes for these ranges;
+ * `src_bytes` must be at least that) into microbatch `mb` of `dst`.  Only the
+ * streamed positions are written; every other byte of the cache is left as
+ * it was.  The receiver layout may differ from the sender's (capacity,
+ * dense vs paged vs split-key).  Paged receivers: tables must map distinct
+ * tokens to distinct slots (the same block must not appear twice), else the
+ * result is whichever write lands last; tokens with an unmapped entry are
+ * skipped.  A token increment is streamed in with t0 = pos, t1 = pos + 1.
+ * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_HIP. */
+int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
+                 const int32_t* t1, const void* src, uint64_t src_bytes, void* stream);
+
+/* Microbatch swap-out: copy layers [l0, l1), tokens [t0[b], t1[b]) of device
+ * slot `slot` of `dev` to host microbatch `host_mb` of `host`, at equal
+ * logical coordinates; all other host bytes are left as they were.  Both
+ * caches must be DV_DENSE with equal num_layers, num_heads, head_dim, batch
+ * and elem_bytes (their max_seq may differ); `dev` must be DV_MEM_DEVICE and
+ * `host` DV_MEM_HOST_PINNED (allocated with hipHostMalloc).  The copy runs
+ * on the DMA engines (hipMemcpy2DAsync over the token rows) on `stream`,
+ * so it overlaps kernels on other streams.  Swapping a whole microbatch
+ * passes its valid lengths; the step-t update passes t0 = t, t1 = t + 1.
+ * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_UNSUPPORTED, DV_ERR_HIP. */
+int dv_swap_out(const dv_cache* dev, int32_t slot, const dv_cache* host, int32_t host_mb,
+                int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1, void* stream);
+
+/* Microbatch swap-in (prefetch): the reverse copy, host microbatch
+ * `host_mb` -> device slot `slot`.  Same rules as dv_swap_out. */
+int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev, int32_t slot,
+               int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1, void* stream);
+
+/* Static text for a dv_status value. */
+const char* dv_status_string(int status);
+
+/* DV_API_VERSION of the built library. */
+int dv_api_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DV_H */

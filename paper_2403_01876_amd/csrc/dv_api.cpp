@@ -1,0 +1,448 @@
+// C-ABI entry points: host-side validation, sizing and kernel/DMA dispatch.
+// Everything is checked before the first enqueue, so an error return leaves
+// the streams and all memory untouched.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "../../include/dv.h"
+#include "dv_internal.h"
+
+namespace {
+
+using dv::kSeqPerLaunch;
+
+// A validated view of one microbatch of a cache, sizes in 16-byte units.
+struct View {
+  int kind;
+  int mem;
+  int64_t L, H, D, B, E;
+  int64_t du;        // units per token
+  int64_t cap;       // token capacity per sequence
+  int64_t S;         // dense kinds: max_seq
+  int64_t bs, NB, max_blocks;
+  char* base;
+  const int32_t* bt;
+  uint64_t bytes;    // storage bytes of the microbatch
+};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int view_of(const dv_cache* c, int32_t mb, View* v) {
+  if (!c || !c->mb_base) return DV_ERR_INVALID;
+  if (c->elem_bytes <= 0 || c->num_layers <= 0 || c->num_heads <= 0 || c->head_dim <= 0 ||
+      c->batch <= 0 || c->num_mb <= 0)
+    return DV_ERR_INVALID;
+  if (((int64_t)c->head_dim * c->elem_bytes) % 16 != 0) return DV_ERR_INVALID;
+  if (c->mem != DV_MEM_DEVICE && c->mem != DV_MEM_HOST_PINNED) return DV_ERR_INVALID;
+  v->kind = c->kind;
+  v->mem = c->mem;
+  v->L = c->num_layers;
+  v->H = c->num_heads;
+  v->D = c->head_dim;
+  v->B = c->batch;
+  v->E = c->elem_bytes;
+  v->du = v->D * v->E / 16;
+  v->S = v->bs = v->NB = v->max_blocks = 0;
+  v->bt = nullptr;
+  if (c->kind == DV_DENSE || c->kind == DV_DENSE_KSPLIT) {
+    if (c->max_seq <= 0) return DV_ERR_INVALID;
+    v->S = v->cap = c->max_seq;
+    v->bytes = (uint64_t)v->L * 2 * v->B * v->H * v->S * v->du * 16;
+  } else if (c->kind == DV_PAGED) {
+    if (c->block_size <= 0 || c->num_blocks <= 0 || c->max_blocks <= 0 || !c->block_table)
+      return DV_ERR_INVALID;
+    v->bs = c->block_size;
+    v->NB = c->num_blocks;
+    v->max_blocks = c->max_blocks;
+    v->cap = v->bs * v->max_blocks;
+    v->bytes = (uint64_t)v->L * 2 * v->NB * v->H * v->bs * v->du * 16;
+  } else {
+    return DV_ERR_INVALID;
+  }
+  // Extents whose products the kernels take in 32-bit arithmetic.
+  if (v->cap > (1 << 24) || v->du > (1 << 16) || v->H * v->du > (1 << 20) ||
+      v->cap * v->du > (1ll << 30))
+    return DV_ERR_UNSUPPORTED;
+  if (mb < 0) {  // sizing only, no microbatch
+    v->base = nullptr;
+    return DV_OK;
+  }
+  if (mb >= c->num_mb) return DV_ERR_RANGE;
+  v->base = static_cast<char*>(c->mb_base[mb]);
+  if (!v->base || !aligned16(v->base)) return DV_ERR_INVALID;
+  if (c->kind == DV_PAGED) {
+    v->bt = c->block_table[mb];
+    if (!v->bt) return DV_ERR_INVALID;
+  }
+  return DV_OK;
+}
+
+// Checks the ranges and returns the per-sequence (t0, n) and N.
+int ranges_of(const View& v, int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1,
+              std::vector<int32_t>* r0, std::vector<int32_t>* rn, int64_t* N) {
+  if (!t1) return DV_ERR_INVALID;
+  if (l0 < 0 || l1 < l0 || l1 > v.L) return DV_ERR_RANGE;
+  r0->resize(v.B);
+  rn->resize(v.B);
+  int64_t total = 0;
+  for (int64_t b = 0; b < v.B; ++b) {
+    const int64_t a = t0 ? t0[b] : 0, e = t1[b];
+    if (a < 0 || e < a || e > v.cap) return DV_ERR_RANGE;
+    (*r0)[b] = (int32_t)a;
+    (*rn)[b] = (int32_t)(e - a);
+    total += e - a;
+  }
+  *N = total;
+  return DV_OK;
+}
+
+uint64_t wire_bytes(const View& v, int32_t l0, int32_t l1, int64_t N) {
+  return (uint64_t)(l1 - l0) * 2 * v.H * v.du * 16 * (uint64_t)N;
+}
+
+bool overlaps(const void* a, uint64_t na, const void* b, uint64_t nb) {
+  if (na == 0 || nb == 0) return false;
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+// DV_ERR_HIP for a failed runtime call; with DV_DEBUG set in the environment
+// the runtime's error name is also printed to stderr.
+int hip_fail(hipError_t e, const char* what) {
+  if (e == hipSuccess) return DV_OK;
+  static const bool debug = getenv("DV_DEBUG") != nullptr;
+  if (debug) fprintf(stderr, "libdv: %s failed: %s\n", what, hipGetErrorName(e));
+  return DV_ERR_HIP;
+}
+
+int hip_status(hipError_t e) { return hip_fail(e, "hipMemcpy2DAsync"); }
+
+// Enqueue the pack (dir = kPack) or unpack of the validated ranges.  The wire
+// is at `wire`; per (layer, K|V) slab it holds N*H*du units.
+int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector<int32_t>& t0,
+               const std::vector<int32_t>& n, int64_t N, void* wire, hipStream_t st) {
+  if (N == 0 || l1 == l0) return DV_OK;
+  const int64_t w_slab = N * v.H * v.du;
+  const uint32_t nl = (uint32_t)(l1 - l0);
+  int32_t max_n = 0;
+  for (int32_t x : n) max_n = std::max(max_n, x);
+  const bool single = max_n <= 1;
+
+  int64_t p_group = 0;  // tokens of all earlier launch groups
+  for (int64_t g0 = 0; g0 < v.B; g0 += kSeqPerLaunch) {
+    const int nseq = (int)std::min<int64_t>(kSeqPerLaunch, v.B - g0);
+    int64_t ntok = 0;
+    for (int i = 0; i < nseq; ++i) ntok += n[g0 + i];
+    if (ntok == 0) continue;
+    char* wire_g = static_cast<char*>(wire) + (uint64_t)p_group * v.H * v.du * 16;
+    p_group += ntok;
+
+    dv::SeqRanges r;
+    memset(&r, 0, sizeof r);
+    for (int i = 0; i < nseq; ++i) {
+      r.t0[i] = t0[g0 + i];
+      r.n[i] = n[g0 + i];
+    }
+
+    if (single) {
+      dv::TokenArgs a;
+      memset(&a, 0, sizeof a);
+      a.cache = v.base;
+      a.wire = wire_g;
+      a.bt = v.bt;
+      a.du = (int32_t)v.du;
+      a.heads = (int32_t)v.H;
+      a.nseq = nseq;
+      a.b0 = (int32_t)g0;
+      for (int i = 0; i < kSeqPerLaunch; ++i) a.pos[i] = (i < nseq && r.n[i] == 1) ? r.t0[i] : -1;
+      const uint32_t units = (uint32_t)(ntok * v.H * v.du);
+      hipError_t e;
+      if (v.kind == DV_PAGED) {
+        a.paged = 1;
+        a.block_size = (int32_t)v.bs;
+        a.num_blocks = (int32_t)v.NB;
+        a.max_blocks = (int32_t)v.max_blocks;
+        a.s_slab = v.NB * v.H * v.bs * v.du;
+        a.s_blk = v.H * v.bs * v.du;
+        a.s_h = v.bs * v.du;
+        a.s_tok = v.du;
+        a.s_e = 1;
+        a.m = {2 * l0, 1, 0, 0, w_slab};
+        e = dv::launch_token(dir, a, units, 2 * nl, st);
+      } else {
+        a.s_slab = v.B * v.H * v.S * v.du;
+        a.s_b = v.H * v.S * v.du;
+        a.s_h = v.S * v.du;
+        if (v.kind == DV_DENSE) {
+          a.s_tok = v.du;
+          a.s_e = 1;
+          a.m = {2 * l0, 1, 0, 0, w_slab};
+          e = dv::launch_token(dir, a, units, 2 * nl, st);
+        } else {
+          // split key slabs: groups S units apart, tokens 1 unit apart
+          a.s_tok = 1;
+          a.s_e = v.S;
+          a.m = {2 * l0, 2, 0, 0, w_slab};
+          e = dv::launch_token(dir, a, units, nl, st);
+          if (e == hipSuccess) {
+            a.s_tok = v.du;
+            a.s_e = 1;
+            a.m = {2 * l0 + 1, 2, 1, 0, w_slab};
+            e = dv::launch_token(dir, a, units, nl, st);
+          }
+        }
+      }
+      if (e != hipSuccess) return hip_fail(e, "token kernel launch");
+      continue;
+    }
+
+    if (v.kind == DV_PAGED) {
+      dv::PagedArgs a;
+      memset(&a, 0, sizeof a);
+      a.pool = v.base;
+      a.wire = wire_g;
+      a.bt = v.bt;
+      a.s_slab = v.NB * v.H * v.bs * v.du;
+      a.s_blk = v.H * v.bs * v.du;
+      a.s_h = v.bs * v.du;
+      a.m = {2 * l0, 1, 0, 0, w_slab};
+      a.du = (int32_t)v.du;
+      a.heads = (int32_t)v.H;
+      a.nseq = nseq;
+      a.b0 = (int32_t)g0;
+      a.block_size = (int32_t)v.bs;
+      a.num_blocks = (int32_t)v.NB;
+      a.max_blocks = (int32_t)v.max_blocks;
+      a.r = r;
+      int64_t tiles = 0;
+      for (int i = 0; i < nseq; ++i)
+        if (r.n[i] > 0) tiles += (r.t0[i] + r.n[i] + v.bs - 1) / v.bs - r.t0[i] / v.bs;
+      if (tiles >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
+      const hipError_t e = dv::launch_paged(dir, a, (uint32_t)tiles, 2 * nl, st);
+      if (e != hipSuccess) return hip_fail(e, "paged kernel launch");
+      continue;
+    }
+
+    dv::DenseRunArgs a;
+    memset(&a, 0, sizeof a);
+    a.cache = v.base;
+    a.wire = wire_g;
+    a.s_slab = v.B * v.H * v.S * v.du;
+    a.s_b = v.H * v.S * v.du;
+    a.s_h = v.S * v.du;
+    a.du = (int32_t)v.du;
+    a.heads = (int32_t)v.H;
+    a.nseq = nseq;
+    a.b0 = (int32_t)g0;
+    a.r = r;
+    int64_t tiles = 0;
+    for (int i = 0; i < nseq; ++i)
+      tiles += v.H * (((int64_t)r.n[i] * v.du + dv::kDenseTile - 1) / dv::kDenseTile);
+    if (tiles >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
+    if (v.kind == DV_DENSE) {
+      a.m = {2 * l0, 1, 0, 0, w_slab};
+      const hipError_t e = dv::launch_dense_runs(dir, a, (uint32_t)tiles, 2 * nl, st);
+      if (e != hipSuccess) return hip_fail(e, "dense kernel launch");
+      continue;
+    }
+    // split key: value slabs are dense runs, key slabs go through LDS
+    a.m = {2 * l0 + 1, 2, 1, 0, w_slab};
+    hipError_t e = dv::launch_dense_runs(dir, a, (uint32_t)tiles, nl, st);
+    if (e != hipSuccess) return hip_fail(e, "dense kernel launch");
+    dv::KsplitArgs k;
+    memset(&k, 0, sizeof k);
+    k.cache = v.base;
+    k.wire = wire_g;
+    k.s_slab = a.s_slab;
+    k.s_b = a.s_b;
+    k.s_h = a.s_h;
+    k.m = {2 * l0, 2, 0, 0, w_slab};
+    k.du = (int32_t)v.du;
+    k.heads = (int32_t)v.H;
+    k.nseq = nseq;
+    k.b0 = (int32_t)g0;
+    k.seq_cap = (int32_t)v.S;
+    k.r = r;
+    int64_t ktiles = 0;
+    for (int i = 0; i < nseq; ++i)
+      ktiles += v.H * (((int64_t)r.n[i] + dv::kKsplitTile - 1) / dv::kKsplitTile);
+    e = dv::launch_ksplit(dir, k, (uint32_t)ktiles, nl, st);
+    if (e != hipSuccess) return hip_fail(e, "split-key kernel launch");
+  }
+  return DV_OK;
+}
+
+int check_kind_supported(const View& v) {
+  if (v.kind == DV_DENSE_KSPLIT && (16 % v.E != 0 || v.du > dv::kKsplitMaxDu))
+    return DV_ERR_UNSUPPORTED;
+  return DV_OK;
+}
+
+int stream_out(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
+               const int32_t* t1, void* dst, uint64_t dst_cap, uint64_t* out_bytes,
+               void* stream) {
+  View v;
+  int rc = view_of(src, mb, &v);
+  if (rc != DV_OK) return rc;
+  std::vector<int32_t> r0, rn;
+  int64_t N = 0;
+  rc = ranges_of(v, l0, l1, t0, t1, &r0, &rn, &N);
+  if (rc != DV_OK) return rc;
+  const uint64_t need = wire_bytes(v, l0, l1, N);
+  if (out_bytes) *out_bytes = need;
+  if (need > dst_cap) return DV_ERR_SPACE;
+  if (need == 0) return DV_OK;
+  if (!dst || !aligned16(dst)) return DV_ERR_INVALID;
+  if (overlaps(dst, need, v.base, v.bytes)) return DV_ERR_INVALID;
+  rc = check_kind_supported(v);
+  if (rc != DV_OK) return rc;
+  return run_stream(dv::kPack, v, l0, l1, r0, rn, N, dst, static_cast<hipStream_t>(stream));
+}
+
+// Copy rows of the validated ranges between two dense caches with DMA.
+int swap_copy(const dv_cache* from, int32_t from_mb, const dv_cache* to, int32_t to_mb,
+              int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1, void* stream,
+              int from_mem, int to_mem) {
+  View a, b;
+  int rc = view_of(from, from_mb, &a);
+  if (rc != DV_OK) return rc;
+  rc = view_of(to, to_mb, &b);
+  if (rc != DV_OK) return rc;
+  if (a.kind != DV_DENSE || b.kind != DV_DENSE) return DV_ERR_UNSUPPORTED;
+  if (a.L != b.L || a.H != b.H || a.D != b.D || a.B != b.B || a.E != b.E) return DV_ERR_INVALID;
+  if (a.mem != from_mem || b.mem != to_mem) return DV_ERR_INVALID;
+  std::vector<int32_t> r0, rn;
+  int64_t N = 0;
+  rc = ranges_of(a, l0, l1, t0, t1, &r0, &rn, &N);
+  if (rc != DV_OK) return rc;
+  for (int64_t i = 0; i < b.B; ++i)
+    if ((int64_t)r0[i] + rn[i] > b.cap) return DV_ERR_RANGE;
+  if (overlaps(a.base, a.bytes, b.base, b.bytes)) return DV_ERR_INVALID;
+  if (N == 0 || l1 == l0) return DV_OK;
+
+  const hipMemcpyKind kind =
+      from_mem == DV_MEM_DEVICE ? hipMemcpyDeviceToHost : hipMemcpyHostToDevice;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t tok = (size_t)a.du * 16;
+  const size_t ap = (size_t)a.S * tok, bp = (size_t)b.S * tok;  // row pitches
+  bool uniform = true;
+  for (int64_t i = 1; i < a.B; ++i)
+    if (r0[i] != r0[0] || rn[i] != rn[0]) uniform = false;
+  if (uniform) {
+    // Rows (slab, b, h) of the layer range are consecutive at one pitch.
+    const size_t row0 = (size_t)2 * l0 * a.B * a.H;
+    const size_t rows = (size_t)2 * (l1 - l0) * a.B * a.H;
+    return hip_status(hipMemcpy2DAsync(b.base + row0 * bp + r0[0] * tok, bp,
+                                       a.base + row0 * ap + r0[0] * tok, ap, rn[0] * tok, rows,
+                                       kind, st));
+  }
+  for (int64_t slab = 2 * l0; slab < 2 * l1; ++slab) {
+    for (int64_t s = 0; s < a.B; ++s) {
+      if (rn[s] == 0) continue;
+      const size_t row0 = (size_t)(slab * a.B + s) * a.H;
+      hipError_t e = hipMemcpy2DAsync(b.base + row0 * bp + r0[s] * tok, bp,
+                                      a.base + row0 * ap + r0[s] * tok, ap, rn[s] * tok,
+                                      (size_t)a.H, kind, st);
+      if (e != hipSuccess) return hip_fail(e, "hipMemcpy2DAsync");
+    }
+  }
+  return DV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dv_api_version(void) { return DV_API_VERSION; }
+
+const char* dv_status_string(int status) {
+  switch (status) {
+    case DV_OK: return "ok";
+    case DV_ERR_INVALID: return "invalid argument";
+    case DV_ERR_RANGE: return "range outside the cache";
+    case DV_ERR_SPACE: return "buffer too small";
+    case DV_ERR_UNSUPPORTED: return "unsupported layout or size";
+    case DV_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int dv_cache_bytes(const dv_cache* c, uint64_t* out_bytes) {
+  View v;
+  int rc = view_of(c, -1, &v);
+  if (rc != DV_OK) return rc;
+  if (out_bytes) *out_bytes = v.bytes;
+  return DV_OK;
+}
+
+int dv_packed_bytes(const dv_cache* c, int32_t l0, int32_t l1, const int32_t* t0,
+                    const int32_t* t1, uint64_t* out_bytes) {
+  View v;
+  int rc = view_of(c, -1, &v);
+  if (rc != DV_OK) return rc;
+  std::vector<int32_t> r0, rn;
+  int64_t N = 0;
+  rc = ranges_of(v, l0, l1, t0, t1, &r0, &rn, &N);
+  if (rc != DV_OK) return rc;
+  if (out_bytes) *out_bytes = wire_bytes(v, l0, l1, N);
+  return DV_OK;
+}
+
+int dv_stream_out_prompt(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
+                         const int32_t* t0, const int32_t* t1, void* dst, uint64_t dst_cap,
+                         uint64_t* out_bytes, void* stream) {
+  return stream_out(src, mb, l0, l1, t0, t1, dst, dst_cap, out_bytes, stream);
+}
+
+int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
+                        const int32_t* pos, void* dst, uint64_t dst_cap, uint64_t* out_bytes,
+                        void* stream) {
+  if (!src || !pos || src->batch <= 0) return DV_ERR_INVALID;
+  std::vector<int32_t> a(src->batch), e(src->batch);
+  for (int32_t b = 0; b < src->batch; ++b) {
+    a[b] = pos[b] < 0 ? 0 : pos[b];
+    e[b] = pos[b] < 0 ? 0 : pos[b] + 1;
+    if (pos[b] == INT32_MAX) return DV_ERR_RANGE;
+  }
+  return stream_out(src, mb, l0, l1, a.data(), e.data(), dst, dst_cap, out_bytes, stream);
+}
+
+int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
+                 const int32_t* t1, const void* src, uint64_t src_bytes, void* stream) {
+  View v;
+  int rc = view_of(dst, mb, &v);
+  if (rc != DV_OK) return rc;
+  std::vector<int32_t> r0, rn;
+  int64_t N = 0;
+  rc = ranges_of(v, l0, l1, t0, t1, &r0, &rn, &N);
+  if (rc != DV_OK) return rc;
+  const uint64_t need = wire_bytes(v, l0, l1, N);
+  if (src_bytes < need) return DV_ERR_SPACE;
+  if (need == 0) return DV_OK;
+  if (!src || !aligned16(src)) return DV_ERR_INVALID;
+  if (overlaps(src, need, v.base, v.bytes)) return DV_ERR_INVALID;
+  rc = check_kind_supported(v);
+  if (rc != DV_OK) return rc;
+  return run_stream(dv::kUnpack, v, l0, l1, r0, rn, N, const_cast<void*>(src),
+                    static_cast<hipStream_t>(stream));
+}
+
+int dv_swap_out(const dv_cache* dev, int32_t slot, const dv_cache* host, int32_t host_mb,
+                int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1, void* stream) {
+  return swap_copy(dev, slot, host, host_mb, l0, l1, t0, t1, stream, DV_MEM_DEVICE,
+                   DV_MEM_HOST_PINNED);
+}
+
+int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev, int32_t slot,
+               int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1, void* stream) {
+  return swap_copy(host, host_mb, dev, slot, l0, l1, t0, t1, stream, DV_MEM_HOST_PINNED,
+                   DV_MEM_DEVICE);
+}
+
+}  // extern "C"

@@ -1,0 +1,110 @@
+// Internal launch descriptors shared by the host dispatch (dv_api.cpp) and
+// the kernels (dv_kernels.hip).  Units are 16 bytes throughout: every cache
+// and wire address handled here is a multiple of 16 bytes, which lets each
+// lane move one 128-bit word per access.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dv {
+
+// Sequences handled by one launch: one per lane of a 64-wide wavefront, so
+// per-sequence prefix sums are a single wavefront scan.
+constexpr int kSeqPerLaunch = 64;
+constexpr int kThreads = 256;
+
+enum Dir : int { kPack = 0, kUnpack = 1 };
+
+struct SeqRanges {
+  int32_t t0[kSeqPerLaunch];  // first token of each sequence's range
+  int32_t n[kSeqPerLaunch];   // tokens in the range (0 = sequence skipped)
+};
+
+// Slab = one (layer, K|V) half of the cache; grid row y handles cache slab
+// slab0 + y*slab_step, whose data sits in wire slab wslab0 + y*slab_step.
+struct SlabMap {
+  int32_t slab0, slab_step, wslab0, pad;
+  int64_t w_slab;  // wire units per slab: N * heads * du
+};
+
+// Dense runs: for each (sequence, head) the range is one contiguous run of
+// n*du units in the cache and in the wire.
+struct DenseRunArgs {
+  void* cache;     // microbatch base
+  void* wire;      // wire base advanced to this launch's first sequence
+  int64_t s_slab;  // cache units per slab
+  int64_t s_b;     // cache units per sequence
+  int64_t s_h;     // cache units per head
+  SlabMap m;
+  int32_t du;      // units per token (head_dim * elem_bytes / 16)
+  int32_t heads;
+  int32_t nseq;    // sequences in this launch (<= 64)
+  int32_t b0;      // index of the launch's first sequence
+  SeqRanges r;
+};
+
+// Paged blocks: one workgroup per (slab, sequence, logical block).
+struct PagedArgs {
+  void* pool;
+  void* wire;
+  const int32_t* bt;  // this microbatch's block table [batch][max_blocks]
+  int64_t s_slab;     // pool units per slab (NB * heads * bs * du)
+  int64_t s_blk;      // pool units per block (heads * bs * du)
+  int64_t s_h;        // pool units per head in a block (bs * du)
+  SlabMap m;
+  int32_t du, heads, nseq, b0;
+  int32_t block_size, num_blocks, max_blocks, pad;
+  SeqRanges r;
+};
+
+// Single-token ranges (decode-step increments): one unit per lane over the
+// flattened (active sequence, head, unit) space of each slab.
+struct TokenArgs {
+  void* cache;
+  void* wire;
+  const int32_t* bt;  // paged only
+  int64_t s_slab;
+  int64_t s_b;        // dense: units per sequence
+  int64_t s_blk;      // paged: units per block
+  int64_t s_h;        // units per head (dense: S*du; paged: bs*du; split key: S*du)
+  int64_t s_tok;      // units per token (du, or 1 in a split key slab)
+  int64_t s_e;        // units between consecutive 16-byte groups of one token
+                      // (1, or S in a split key slab)
+  SlabMap m;
+  int32_t du, heads, nseq, b0;
+  int32_t paged, block_size, num_blocks, max_blocks;
+  int32_t pos[kSeqPerLaunch];  // token of each sequence, < 0 = inactive
+};
+
+// Split-key slab: 64-token tiles transposed through LDS.
+struct KsplitArgs {
+  void* cache;
+  void* wire;
+  int64_t s_slab, s_b, s_h;  // as dense
+  SlabMap m;
+  int32_t du;  // 16-byte groups per token (head_dim * elem_bytes / 16), <= kKsplitMaxDu
+  int32_t heads, nseq, b0;
+  int32_t seq_cap;  // S: units between consecutive groups of one head
+  int32_t pad;
+  SeqRanges r;
+};
+constexpr int kKsplitTile = 64;
+constexpr int kKsplitMaxDu = 32;
+
+// Launchers (dv_kernels.hip).  Each returns the hipError_t of its launch.
+hipError_t launch_dense_runs(int dir, const DenseRunArgs& a, uint32_t tiles_per_slab,
+                             uint32_t nslabs, hipStream_t s);
+hipError_t launch_paged(int dir, const PagedArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,
+                        hipStream_t s);
+hipError_t launch_token(int dir, const TokenArgs& a, uint32_t units_per_slab, uint32_t nslabs,
+                        hipStream_t s);
+hipError_t launch_ksplit(int dir, const KsplitArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,
+                         hipStream_t s);
+
+// Units each dense-run workgroup moves (tiles are counted on the host with
+// the same constant).
+constexpr int kDenseUnroll = 8;
+constexpr int kDenseTile = kThreads * kDenseUnroll;
+
+}  // namespace dv

@@ -1,0 +1,321 @@
+// Pack / unpack kernels for gfx950.  Pure data movement: every lane moves
+// 16-byte words with nontemporal global loads and stores (the data is
+// streamed once, so it should not displace L2/MALL contents), no arithmetic
+// touches the payload and no MFMA is involved.
+//
+// Work resolution: a launch covers at most 64 sequences, one per lane of a
+// wavefront.  Each workgroup recomputes, with one 64-lane inclusive scan, the
+// prefix of per-sequence tile counts and token counts; a ballot of
+// "prefix <= my tile" then gives the workgroup's sequence directly.  The
+// per-sequence ranges travel by value in the kernel arguments, so nothing is
+// copied to the device before a launch.
+#include "dv_internal.h"
+
+namespace dv {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4 ld_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void st_nt(u32x4 v, u32x4* p) { __builtin_nontemporal_store(v, p); }
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+// Inclusive prefix sum across the 64 lanes of a wavefront.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(v, o, 64);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+// Index of the first lane whose inclusive prefix exceeds `item` (prefixes
+// are non-decreasing across lanes, so the lanes at or below `item` form a
+// prefix of the wavefront).
+__device__ __forceinline__ int owner_lane(int incl, int item) {
+  return __popcll(__ballot(incl <= item));
+}
+
+// ---------------------------------------------------------------------------
+// Dense runs: grid (tiles_per_slab, nslabs); a tile is kDenseTile units of
+// one (sequence, head) run.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ void __launch_bounds__(kThreads) dense_runs_kernel(DenseRunArgs a) {
+  const int lane = lane_id();
+  int n = 0, t0 = 0;
+  if (lane < a.nseq) {
+    n = a.r.n[lane];
+    t0 = a.r.t0[lane];
+  }
+  const int run = n * a.du;
+  const int tpr = (run + kDenseTile - 1) / kDenseTile;
+  const int tiles = tpr * a.heads;
+  const int incl = wave_incl_scan(tiles);
+  const int tok_incl = wave_incl_scan(n);
+
+  const int tile = blockIdx.x;
+  const int b = owner_lane(incl, tile);
+  const int excl_b = __shfl(incl - tiles, b, 64);
+  const int tpr_b = __shfl(tpr, b, 64);
+  const int run_b = __shfl(run, b, 64);
+  const int t0_b = __shfl(t0, b, 64);
+  const int p_b = __shfl(tok_incl - n, b, 64);
+
+  const int r = tile - excl_b;
+  const int h = r / tpr_b;
+  const int k = r - h * tpr_b;
+
+  const int64_t y = blockIdx.y;
+  const int64_t slab = a.m.slab0 + y * a.m.slab_step;
+  const int64_t wslab = a.m.wslab0 + y * a.m.slab_step;
+  u32x4* cache = (u32x4*)a.cache + slab * a.s_slab + (int64_t)(a.b0 + b) * a.s_b +
+                 (int64_t)h * a.s_h + (int64_t)t0_b * a.du + (int64_t)k * kDenseTile;
+  u32x4* wire = (u32x4*)a.wire + wslab * a.m.w_slab + (int64_t)p_b * a.heads * a.du +
+                (int64_t)h * run_b + (int64_t)k * kDenseTile;
+  const u32x4* src = (D == kPack) ? cache : wire;
+  u32x4* dst = (D == kPack) ? wire : cache;
+  const int count = min(kDenseTile, run_b - k * kDenseTile);
+
+  u32x4 v[kDenseUnroll];
+#pragma unroll
+  for (int i = 0; i < kDenseUnroll; ++i) {
+    const int idx = i * kThreads + threadIdx.x;
+    if (idx < count) v[i] = ld_nt(src + idx);
+  }
+#pragma unroll
+  for (int i = 0; i < kDenseUnroll; ++i) {
+    const int idx = i * kThreads + threadIdx.x;
+    if (idx < count) st_nt(v[i], dst + idx);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Paged blocks: grid (tiles_per_slab, nslabs); a tile is the part of one
+// logical block of one sequence inside its token range, all heads.  For a
+// fixed (slab, block) the pool holds the heads back to back, so a full
+// block is heads*bs*du contiguous units.
+// ---------------------------------------------------------------------------
+constexpr int kPagedHeadUnroll = 8;
+
+template <int D>
+__global__ void __launch_bounds__(kThreads) paged_kernel(PagedArgs a) {
+  const int lane = lane_id();
+  const int bs = a.block_size;
+  int n = 0, t0 = 0, nblk = 0;
+  if (lane < a.nseq) {
+    n = a.r.n[lane];
+    t0 = a.r.t0[lane];
+    if (n > 0) nblk = (t0 + n + bs - 1) / bs - t0 / bs;
+  }
+  const int incl = wave_incl_scan(nblk);
+  const int tok_incl = wave_incl_scan(n);
+
+  const int tile = blockIdx.x;
+  const int b = owner_lane(incl, tile);
+  const int excl_b = __shfl(incl - nblk, b, 64);
+  const int n_b = __shfl(n, b, 64);
+  const int t0_b = __shfl(t0, b, 64);
+  const int p_b = __shfl(tok_incl - n, b, 64);
+
+  const int j = t0_b / bs + (tile - excl_b);
+  const int s_lo = max(t0_b, j * bs);
+  const int s_hi = min(t0_b + n_b, (j + 1) * bs);
+  const int blk = a.bt[(int64_t)(a.b0 + b) * a.max_blocks + j];
+  if (blk < 0 || blk >= a.num_blocks) return;  // unmapped block: skipped
+
+  const int run = (s_hi - s_lo) * a.du;  // units per head in this tile
+  const int64_t y = blockIdx.y;
+  const int64_t slab = a.m.slab0 + y * a.m.slab_step;
+  const int64_t wslab = a.m.wslab0 + y * a.m.slab_step;
+  u32x4* pool = (u32x4*)a.pool + slab * a.s_slab + (int64_t)blk * a.s_blk +
+                (int64_t)(s_lo - j * bs) * a.du;
+  u32x4* wire = (u32x4*)a.wire + wslab * a.m.w_slab + (int64_t)p_b * a.heads * a.du +
+                (int64_t)(s_lo - t0_b) * a.du;
+  const int64_t w_h = (int64_t)n_b * a.du;  // wire units per head of this sequence
+
+  for (int h0 = 0; h0 < a.heads; h0 += kPagedHeadUnroll) {
+    for (int e = threadIdx.x; e < run; e += kThreads) {
+      u32x4 v[kPagedHeadUnroll];
+#pragma unroll
+      for (int i = 0; i < kPagedHeadUnroll; ++i) {
+        const int h = h0 + i;
+        if (h < a.heads) {
+          const u32x4* src = (D == kPack) ? pool + h * a.s_h + e : wire + h * w_h + e;
+          v[i] = ld_nt(src);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kPagedHeadUnroll; ++i) {
+        const int h = h0 + i;
+        if (h < a.heads) {
+          u32x4* dst = (D == kPack) ? wire + h * w_h + e : pool + h * a.s_h + e;
+          st_nt(v[i], dst);
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Single tokens: grid (ceil(units_per_slab / 256), nslabs).  Lane u of a
+// slab moves wire unit u; the active sequences are ranked once per
+// workgroup into LDS together with the cache offset of their token.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ void __launch_bounds__(kThreads) token_kernel(TokenArgs a) {
+  __shared__ int64_t s_base[kSeqPerLaunch];
+  const int lane = lane_id();
+  const int p = lane < a.nseq ? a.pos[lane] : -1;
+  const uint64_t act = __ballot(p >= 0);
+  const int nact = __popcll(act);
+  if (threadIdx.x < 64 && p >= 0) {
+    const int rank = __popcll(act & ((1ull << lane) - 1ull));
+    const int b = a.b0 + lane;
+    int64_t base;
+    if (!a.paged) {
+      base = (int64_t)b * a.s_b + (int64_t)p * a.s_tok;
+    } else {
+      const int blk = a.bt[(int64_t)b * a.max_blocks + p / a.block_size];
+      base = (blk >= 0 && blk < a.num_blocks)
+                 ? (int64_t)blk * a.s_blk + (int64_t)(p % a.block_size) * a.s_tok
+                 : -1;
+    }
+    s_base[rank] = base;
+  }
+  __syncthreads();
+
+  const int hd = a.heads * a.du;
+  const int u = blockIdx.x * kThreads + threadIdx.x;
+  if (u >= nact * hd) return;
+  const int rank = u / hd;
+  const int rem = u - rank * hd;
+  const int h = rem / a.du;
+  const int e = rem - h * a.du;
+  const int64_t base = s_base[rank];
+  if (base < 0) return;  // unmapped block: skipped
+
+  const int64_t y = blockIdx.y;
+  const int64_t slab = a.m.slab0 + y * a.m.slab_step;
+  const int64_t wslab = a.m.wslab0 + y * a.m.slab_step;
+  u32x4* cache = (u32x4*)a.cache + slab * a.s_slab + base + (int64_t)h * a.s_h +
+                 (int64_t)e * a.s_e;
+  u32x4* wire = (u32x4*)a.wire + wslab * a.m.w_slab + u;
+  if (D == kPack)
+    st_nt(ld_nt(cache), wire);
+  else
+    st_nt(ld_nt(wire), cache);
+}
+
+// ---------------------------------------------------------------------------
+// Split-key slab: grid (tiles_per_slab, nslabs); a tile is 64 tokens of one
+// (sequence, head).  The cache holds the head as [group][token] (each group
+// 16 bytes), the wire as [token][group]: the tile is read with lanes along
+// the contiguous axis of the source, transposed through LDS, and written
+// with lanes along the contiguous axis of the destination.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ void __launch_bounds__(kThreads) ksplit_kernel(KsplitArgs a) {
+  // one padding unit per row keeps the column accesses on distinct banks
+  __shared__ u32x4 tileL[kKsplitTile][kKsplitMaxDu + 1];
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  int n = 0, t0 = 0;
+  if (lane < a.nseq) {
+    n = a.r.n[lane];
+    t0 = a.r.t0[lane];
+  }
+  const int tpr = (n + kKsplitTile - 1) / kKsplitTile;
+  const int tiles = tpr * a.heads;
+  const int incl = wave_incl_scan(tiles);
+  const int tok_incl = wave_incl_scan(n);
+
+  const int tile = blockIdx.x;
+  const int b = owner_lane(incl, tile);
+  const int excl_b = __shfl(incl - tiles, b, 64);
+  const int tpr_b = __shfl(tpr, b, 64);
+  const int n_b = __shfl(n, b, 64);
+  const int t0_b = __shfl(t0, b, 64);
+  const int p_b = __shfl(tok_incl - n, b, 64);
+  const int r = tile - excl_b;
+  const int h = r / tpr_b;
+  const int k = r - h * tpr_b;
+  const int tok0 = k * kKsplitTile;                  // first token of the tile, range-relative
+  const int ntk = min(kKsplitTile, n_b - tok0);      // tokens in the tile
+  const int du = a.du;
+
+  const int64_t y = blockIdx.y;
+  const int64_t slab = a.m.slab0 + y * a.m.slab_step;
+  const int64_t wslab = a.m.wslab0 + y * a.m.slab_step;
+  u32x4* head = (u32x4*)a.cache + slab * a.s_slab + (int64_t)(a.b0 + b) * a.s_b +
+                (int64_t)h * a.s_h + t0_b + tok0;  // group 0 of the tile's first token
+  u32x4* wire = (u32x4*)a.wire + wslab * a.m.w_slab + (int64_t)p_b * a.heads * du +
+                (int64_t)h * n_b * du + (int64_t)tok0 * du;
+  const int64_t S = a.seq_cap;
+
+  if (D == kPack) {
+    for (int g = wave; g < du; g += kThreads / 64)
+      if (lane < ntk) tileL[lane][g] = ld_nt(head + g * S + lane);
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < ntk * du; idx += kThreads) {
+      const int t = idx / du, g = idx - t * du;
+      st_nt(tileL[t][g], wire + idx);
+    }
+  } else {
+    for (int idx = threadIdx.x; idx < ntk * du; idx += kThreads) {
+      const int t = idx / du, g = idx - t * du;
+      tileL[t][g] = ld_nt(wire + idx);
+    }
+    __syncthreads();
+    for (int g = wave; g < du; g += kThreads / 64)
+      if (lane < ntk) st_nt(tileL[lane][g], head + g * S + lane);
+  }
+}
+
+}  // namespace
+
+namespace {
+
+// Launch with the runtime's own status for this launch (a stale error left by
+// an unrelated earlier call is not picked up, unlike hipGetLastError).
+template <typename Args>
+hipError_t launch(const void* fn, dim3 grid, const Args& a, hipStream_t s) {
+  if (grid.x == 0 || grid.y == 0) return hipSuccess;
+  void* args[] = {const_cast<Args*>(&a)};
+  return hipLaunchKernel(fn, grid, dim3(kThreads), args, 0, s);
+}
+
+}  // namespace
+
+hipError_t launch_dense_runs(int dir, const DenseRunArgs& a, uint32_t tiles_per_slab,
+                             uint32_t nslabs, hipStream_t s) {
+  const void* fn = dir == kPack ? (const void*)&dense_runs_kernel<kPack>
+                                : (const void*)&dense_runs_kernel<kUnpack>;
+  return launch(fn, dim3(tiles_per_slab, nslabs), a, s);
+}
+
+hipError_t launch_paged(int dir, const PagedArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,
+                        hipStream_t s) {
+  const void* fn =
+      dir == kPack ? (const void*)&paged_kernel<kPack> : (const void*)&paged_kernel<kUnpack>;
+  return launch(fn, dim3(tiles_per_slab, nslabs), a, s);
+}
+
+hipError_t launch_token(int dir, const TokenArgs& a, uint32_t units_per_slab, uint32_t nslabs,
+                        hipStream_t s) {
+  const void* fn =
+      dir == kPack ? (const void*)&token_kernel<kPack> : (const void*)&token_kernel<kUnpack>;
+  return launch(fn, dim3((units_per_slab + kThreads - 1) / kThreads, nslabs), a, s);
+}
+
+hipError_t launch_ksplit(int dir, const KsplitArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,
+                         hipStream_t s) {
+  const void* fn =
+      dir == kPack ? (const void*)&ksplit_kernel<kPack> : (const void*)&ksplit_kernel<kUnpack>;
+  return launch(fn, dim3(tiles_per_slab, nslabs), a, s);
+}
+
+}  // namespace dv

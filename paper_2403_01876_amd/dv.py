@@ -1,0 +1,211 @@
+"""Python binding of ``libdv.so`` (ctypes): argument marshalling only.
+
+The functions carry the C names (``dv_stream_out_prompt`` ...) and take the
+same arguments; buffers may be given as raw addresses or as tensors (their
+``data_ptr()`` is passed), streams as raw ``hipStream_t`` values or
+``torch.cuda.Stream`` objects.  Every byte is moved by the library's HIP
+kernels or DMA calls; there is no Python or CPU fallback, and importing this
+module fails loudly if the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdv.so")
+
+DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_UNSUPPORTED, DV_ERR_HIP = \
+    0, -1, -2, -3, -4, -5
+DV_DENSE, DV_PAGED, DV_DENSE_KSPLIT = 0, 1, 2
+DV_MEM_DEVICE, DV_MEM_HOST_PINNED = 0, 1
+
+
+class DvError(RuntimeError):
+    def __init__(self, status: int, call: str):
+        super().__init__(f"{call}: {status_string(status)} ({status})")
+        self.status = status
+
+
+class dv_cache(ctypes.Structure):
+    _fields_ = [
+        ("kind", ctypes.c_int32),
+        ("mem", ctypes.c_int32),
+        ("elem_bytes", ctypes.c_int32),
+        ("num_layers", ctypes.c_int32),
+        ("num_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("batch", ctypes.c_int32),
+        ("max_seq", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("num_blocks", ctypes.c_int32),
+        ("max_blocks", ctypes.c_int32),
+        ("num_mb", ctypes.c_int32),
+        ("mb_base", ctypes.POINTER(ctypes.c_void_p)),
+        ("block_table", ctypes.POINTER(ctypes.c_void_p)),
+    ]
+
+
+def _load():
+    # torch's libraries need the HIP runtime by file name (libamdhip64.so)
+    # while libdv.so needs it by SONAME (libamdhip64.so.7): importing torch
+    # first makes libdv.so bind to the runtime torch already loaded, so both
+    # share one runtime (a second copy in the process sees no device).
+    import torch  # noqa: F401
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER(dv_cache)
+    i32, u64, vp = ctypes.c_int32, ctypes.c_uint64, ctypes.c_void_p
+    u64p = ctypes.POINTER(ctypes.c_uint64)
+    sig = {
+        "dv_cache_bytes": [P, u64p],
+        "dv_packed_bytes": [P, i32, i32, vp, vp, u64p],
+        "dv_stream_out_prompt": [P, i32, i32, i32, vp, vp, vp, u64, u64p, vp],
+        "dv_stream_out_token": [P, i32, i32, i32, vp, vp, u64, u64p, vp],
+        "dv_stream_in": [P, i32, i32, i32, vp, vp, vp, u64, vp],
+        "dv_swap_out": [P, i32, P, i32, i32, i32, vp, vp, vp],
+        "dv_swap_in": [P, i32, P, i32, i32, i32, vp, vp, vp],
+        "dv_api_version": [],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = ctypes.c_int
+    lib.dv_status_string.argtypes = [ctypes.c_int]
+    lib.dv_status_string.restype = ctypes.c_char_p
+    return lib
+
+
+lib = _load()
+
+# Symbols include/dv.h declares (checked by the tests against the library).
+EXPORTS = ("dv_cache_bytes", "dv_packed_bytes", "dv_stream_out_prompt", "dv_stream_out_token",
+           "dv_stream_in", "dv_swap_out", "dv_swap_in", "dv_status_string", "dv_api_version")
+
+
+def status_string(status: int) -> str:
+    return lib.dv_status_string(status).decode()
+
+
+def _addr(x) -> int:
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    raise TypeError(f"cannot take the address of {type(x)}")
+
+
+def _stream(s) -> int:
+    if s is None:
+        return 0
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+class Cache:
+    """A ``dv_cache`` descriptor plus the host arrays it points to."""
+
+    def __init__(self, kind: int, layers: int, heads: int, head_dim: int, batch: int,
+                 bases: Sequence, max_seq: int = 0, elem_bytes: int = 2,
+                 mem: int = DV_MEM_DEVICE, block_size: int = 0, num_blocks: int = 0,
+                 max_blocks: int = 0, block_tables: Optional[Sequence] = None):
+        self.bases = (ctypes.c_void_p * len(bases))(*[_addr(b) for b in bases])
+        self.tables = None
+        if block_tables is not None:
+            self.tables = (ctypes.c_void_p * len(block_tables))(*[_addr(t) for t in block_tables])
+        self.c = dv_cache(kind, mem, elem_bytes, layers, heads, head_dim, batch, max_seq,
+                          block_size, num_blocks, max_blocks, len(bases),
+                          ctypes.cast(self.bases, ctypes.POINTER(ctypes.c_void_p)),
+                          None if self.tables is None else
+                          ctypes.cast(self.tables, ctypes.POINTER(ctypes.c_void_p)))
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+def _i32(a):
+    if a is None:
+        return None, 0
+    arr = np.ascontiguousarray(a, dtype=np.int32)
+    return arr, arr.ctypes.data
+
+
+def _check(rc: int, name: str, check: bool):
+    if check and rc != DV_OK:
+        raise DvError(rc, name)
+    return rc
+
+
+def dv_cache_bytes(cache: Cache) -> int:
+    out = ctypes.c_uint64(0)
+    _check(lib.dv_cache_bytes(cache.ref, ctypes.byref(out)), "dv_cache_bytes", True)
+    return out.value
+
+
+def dv_packed_bytes(cache: Cache, l0: int, l1: int, t0, t1, check: bool = True):
+    a0, p0 = _i32(t0)
+    a1, p1 = _i32(t1)
+    out = ctypes.c_uint64(0)
+    rc = lib.dv_packed_bytes(cache.ref, l0, l1, p0, p1, ctypes.byref(out))
+    _check(rc, "dv_packed_bytes", check)
+    return out.value if check else (rc, out.value)
+
+
+def dv_stream_out_prompt(src: Cache, mb: int, l0: int, l1: int, t0, t1, dst, dst_cap: int,
+                         stream=None, check: bool = True):
+    """Returns the stream size in bytes (or ``(status, bytes)`` with check=False)."""
+    a0, p0 = _i32(t0)
+    a1, p1 = _i32(t1)
+    out = ctypes.c_uint64(0)
+    rc = lib.dv_stream_out_prompt(src.ref, mb, l0, l1, p0, p1, _addr(dst), dst_cap,
+                                  ctypes.byref(out), _stream(stream))
+    _check(rc, "dv_stream_out_prompt", check)
+    return out.value if check else (rc, out.value)
+
+
+def dv_stream_out_token(src: Cache, mb: int, l0: int, l1: int, pos, dst, dst_cap: int,
+                        stream=None, check: bool = True):
+    ap, pp = _i32(pos)
+    out = ctypes.c_uint64(0)
+    rc = lib.dv_stream_out_token(src.ref, mb, l0, l1, pp, _addr(dst), dst_cap,
+                                 ctypes.byref(out), _stream(stream))
+    _check(rc, "dv_stream_out_token", check)
+    return out.value if check else (rc, out.value)
+
+
+def dv_stream_in(dst: Cache, mb: int, l0: int, l1: int, t0, t1, src, src_bytes: int,
+                 stream=None, check: bool = True) -> int:
+    a0, p0 = _i32(t0)
+    a1, p1 = _i32(t1)
+    rc = lib.dv_stream_in(dst.ref, mb, l0, l1, p0, p1, _addr(src), src_bytes, _stream(stream))
+    return _check(rc, "dv_stream_in", check)
+
+
+def dv_swap_out(dev: Cache, slot: int, host: Cache, host_mb: int, l0: int, l1: int, t0, t1,
+                stream=None, check: bool = True) -> int:
+    a0, p0 = _i32(t0)
+    a1, p1 = _i32(t1)
+    rc = lib.dv_swap_out(dev.ref, slot, host.ref, host_mb, l0, l1, p0, p1, _stream(stream))
+    return _check(rc, "dv_swap_out", check)
+
+
+def dv_swap_in(host: Cache, host_mb: int, dev: Cache, slot: int, l0: int, l1: int, t0, t1,
+               stream=None, check: bool = True) -> int:
+    a0, p0 = _i32(t0)
+    a1, p1 = _i32(t1)
+    rc = lib.dv_swap_in(host.ref, host_mb, dev.ref, slot, l0, l1, p0, p1, _stream(stream))
+    return _check(rc, "dv_swap_in", check)
+
+
+def dv_api_version() -> int:
+    return lib.dv_api_version()

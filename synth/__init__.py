@@ -96,7 +96,19 @@ def words_u64(seed: int, first_word: int, count: int) -> np.ndarray:
 
 
 def fill_bytes(nbytes: int, seed: int, first_byte: int = 0) -> np.ndarray:
-    """Host fill: ``nbytes`` bytes of the counter-mode stream from ``first_byte``."""
+    """Host fill: ``nbytes`` bytes of the counter-mode stream from ``first_byte``.
+
+    Uses the C twin (``csrc/gen_host.c``) when it is built, else numpy."""
+    lib = _host_lib()
+    if lib is not None:
+        out = np.empty(nbytes, dtype=np.uint8)
+        lib.dvsynth_host_fill(out.ctypes.data, nbytes, seed & MASK64, first_byte)
+        return out
+    return fill_bytes_numpy(nbytes, seed, first_byte)
+
+
+def fill_bytes_numpy(nbytes: int, seed: int, first_byte: int = 0) -> np.ndarray:
+    """The numpy statement of the same definition (reference for the C twin)."""
     w0 = first_byte // 8
     w1 = (first_byte + nbytes + 7) // 8
     words = words_u64(seed, w0, w1 - w0)
@@ -122,6 +134,35 @@ def bytes_at(seed: int, byte_index: np.ndarray, width: int) -> np.ndarray:
         z = z ^ (z >> np.uint64(31))
     mask = np.uint64((1 << (8 * width)) - 1) if width < 8 else np.uint64(MASK64)
     return (z >> shift) & mask
+
+
+_HOST_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdvsynth_host.so")
+_host = None
+
+
+def build_host(out: str = _HOST_LIB_PATH) -> str:
+    """Compile the host fill with gcc."""
+    import subprocess
+    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "gen_host.c")
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", src, "-o", out], check=True)
+    return out
+
+
+def _host_lib():
+    global _host
+    if _host is None:
+        if not os.path.exists(_HOST_LIB_PATH):
+            try:
+                build_host()
+            except Exception:  # no compiler: numpy path
+                _host = False
+                return None
+        lib = ctypes.CDLL(_HOST_LIB_PATH)
+        lib.dvsynth_host_fill.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
+                                          ctypes.c_uint64]
+        lib.dvsynth_host_fill.restype = None
+        _host = lib
+    return _host or None
 
 
 # ---------------------------------------------------------------------------
@@ -259,6 +300,7 @@ def libsynth():
     """Load the device fill library built from ``synth/csrc/gen_fill.hip``."""
     global _libsynth
     if _libsynth is None:
+        import torch  # noqa: F401  (bind to the HIP runtime torch loaded)
         if not os.path.exists(LIBSYNTH_PATH):
             raise RuntimeError(f"{LIBSYNTH_PATH} is not built; run __graft_entry__.build()")
         lib = ctypes.CDLL(LIBSYNTH_PATH)

@@ -1,0 +1,163 @@
+"""The C-ABI library without a GPU: it loads, exports what include/dv.h
+declares, sizes streams as the oracle does, and rejects bad arguments before
+enqueuing anything (no call here reaches the HIP runtime)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2403_01876_amd import dv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "dv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dv_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = header_functions()
+    assert set(names) == set(dv.EXPORTS), names
+    lib = ctypes.CDLL(dv.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert dv.dv_api_version() == 1
+
+
+def test_status_strings():
+    for s in (0, -1, -2, -3, -4, -5):
+        assert dv.status_string(s) and dv.status_string(s) != "unknown status"
+    assert dv.status_string(-99) == "unknown status"
+
+
+FAKE = 1 << 40  # an aligned address never dereferenced by the host checks
+
+
+def dense(L=2, H=3, D=64, B=4, S=50, E=2, bases=(FAKE,), kind=dv.DV_DENSE, mem=dv.DV_MEM_DEVICE):
+    return dv.Cache(kind, L, H, D, B, list(bases), max_seq=S, elem_bytes=E, mem=mem)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_packed_bytes_matches_oracle(seed, oracle_lib):
+    r = np.random.default_rng(seed)
+    L, H, B, S = int(r.integers(1, 5)), int(r.integers(1, 9)), int(r.integers(1, 80)), \
+        int(r.integers(1, 300))
+    E = int(r.choice([1, 2, 4]))
+    D = int(r.choice([16, 32, 64, 128])) // E * E
+    D = max(D - D % (16 // E), 16 // E)
+    c = dense(L, H, D, B, S, E)
+    lay = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S, elem_bytes=E)
+    t0 = r.integers(0, S + 1, size=B).astype(np.int32)
+    t1 = np.minimum(t0 + r.integers(0, S + 1, size=B), S).astype(np.int32)
+    l0 = int(r.integers(0, L + 1))
+    l1 = int(r.integers(l0, L + 1))
+    assert dv.dv_packed_bytes(c, l0, l1, t0, t1) == oracle_lib.wire_elems(lay, l0, l1, t0, t1) * E
+    assert dv.dv_cache_bytes(c) == lay.storage_bytes()
+
+
+def test_packed_bytes_paged():
+    bt = np.zeros((4, 10), np.int32)
+    c = dv.Cache(dv.DV_PAGED, 3, 8, 128, 4, [FAKE], block_size=16, num_blocks=30,
+                 max_blocks=10, block_tables=[FAKE])
+    assert dv.dv_cache_bytes(c) == 3 * 2 * 30 * 8 * 16 * 128 * 2
+    t1 = np.array([160, 0, 5, 17], np.int32)
+    assert dv.dv_packed_bytes(c, 0, 3, None, t1) == 3 * 2 * 8 * 128 * 2 * int(t1.sum())
+    rc, _ = dv.dv_packed_bytes(c, 0, 3, None, [161, 0, 0, 0], check=False)
+    assert rc == dv.DV_ERR_RANGE
+    del bt
+
+
+def test_range_errors():
+    c = dense()
+    z = np.zeros(4, np.int32)
+    full = np.full(4, 50, np.int32)
+    assert dv.dv_packed_bytes(c, 0, 2, z, full, check=False)[0] == dv.DV_OK
+    assert dv.dv_packed_bytes(c, 0, 3, z, full, check=False)[0] == dv.DV_ERR_RANGE
+    assert dv.dv_packed_bytes(c, 2, 1, z, full, check=False)[0] == dv.DV_ERR_RANGE
+    assert dv.dv_packed_bytes(c, -1, 1, z, full, check=False)[0] == dv.DV_ERR_RANGE
+    assert dv.dv_packed_bytes(c, 0, 2, z, full + 1, check=False)[0] == dv.DV_ERR_RANGE
+    assert dv.dv_packed_bytes(c, 0, 2, full, z, check=False)[0] == dv.DV_ERR_RANGE
+    assert dv.dv_packed_bytes(c, 0, 2, z - 1, full, check=False)[0] == dv.DV_ERR_RANGE
+    # empty layer range and empty token ranges are valid, zero bytes
+    assert dv.dv_packed_bytes(c, 1, 1, z, full) == 0
+    assert dv.dv_packed_bytes(c, 0, 2, full, full) == 0
+
+
+def test_invalid_descriptors():
+    z = np.zeros(4, np.int32)
+    one = np.ones(4, np.int32)
+    for bad in (dense(D=36), dense(L=0), dense(H=0), dense(B=0), dense(S=0), dense(E=0),
+                dense(kind=7), dense(mem=5)):
+        assert dv.dv_packed_bytes(bad, 0, 1, z, one, check=False)[0] == dv.DV_ERR_INVALID
+    paged_no_table = dv.Cache(dv.DV_PAGED, 1, 1, 64, 4, [FAKE], block_size=16, num_blocks=4,
+                              max_blocks=2)
+    assert dv.dv_packed_bytes(paged_no_table, 0, 1, z, one, check=False)[0] == dv.DV_ERR_INVALID
+
+
+def test_stream_calls_reject_before_enqueue():
+    """Errors return before any HIP call, so they work without a GPU."""
+    c = dense()
+    z = np.zeros(4, np.int32)
+    t1 = np.array([10, 0, 3, 50], np.int32)
+    need = dv.dv_packed_bytes(c, 0, 2, z, t1)
+    rc, n = dv.dv_stream_out_prompt(c, 0, 0, 2, z, t1, FAKE + (1 << 30), need - 16, check=False)
+    assert rc == dv.DV_ERR_SPACE and n == need
+    rc, _ = dv.dv_stream_out_prompt(c, 1, 0, 2, z, t1, FAKE + (1 << 30), need, check=False)
+    assert rc == dv.DV_ERR_RANGE  # microbatch 1 of 1
+    rc, _ = dv.dv_stream_out_prompt(c, 0, 0, 2, z, t1, FAKE + (1 << 30) + 8, need, check=False)
+    assert rc == dv.DV_ERR_INVALID  # misaligned destination
+    rc, _ = dv.dv_stream_out_prompt(c, 0, 0, 2, z, t1, FAKE + 64, need, check=False)
+    assert rc == dv.DV_ERR_INVALID  # destination overlaps the cache
+    rc, _ = dv.dv_stream_out_prompt(c, 0, 0, 2, z, t1, 0, need, check=False)
+    assert rc == dv.DV_ERR_INVALID  # null destination
+    misaligned = dense(bases=(FAKE + 4,))
+    rc, _ = dv.dv_stream_out_prompt(misaligned, 0, 0, 2, z, t1, FAKE + (1 << 30), need,
+                                    check=False)
+    assert rc == dv.DV_ERR_INVALID
+    assert dv.dv_stream_in(c, 0, 0, 2, z, t1, FAKE + (1 << 30), need - 1, check=False) == \
+        dv.DV_ERR_SPACE
+    assert dv.dv_stream_in(c, 0, 0, 2, z, t1 + 50, FAKE + (1 << 30), need,
+                           check=False) == dv.DV_ERR_RANGE
+    pos = np.array([49, -1, 3, 50], np.int32)  # 50 is past capacity
+    rc, _ = dv.dv_stream_out_token(c, 0, 0, 2, pos, FAKE + (1 << 30), 1 << 20, check=False)
+    assert rc == dv.DV_ERR_RANGE
+    # zero-byte streams succeed without touching anything
+    assert dv.dv_stream_out_prompt(c, 0, 0, 2, z, z, 0, 0) == 0
+    assert dv.dv_stream_out_token(c, 0, 0, 2, np.full(4, -1, np.int32), 0, 0) == 0
+    assert dv.dv_stream_in(c, 0, 1, 1, z, t1, 0, 0) == dv.DV_OK
+
+
+def test_ksplit_limits():
+    z = np.zeros(4, np.int32)
+    one = np.ones(4, np.int32) * 2
+    big = dense(D=512, kind=dv.DV_DENSE_KSPLIT)  # 64 groups of 16 bytes per token
+    rc, _ = dv.dv_stream_out_prompt(big, 0, 0, 1, z, one, FAKE + (1 << 34), 1 << 30,
+                                    check=False)
+    assert rc == dv.DV_ERR_UNSUPPORTED
+
+
+def test_swap_rejections():
+    z = np.zeros(4, np.int32)
+    t1 = np.full(4, 10, np.int32)
+    d = dense()
+    h = dense(bases=(FAKE + (1 << 33),), mem=dv.DV_MEM_HOST_PINNED, S=20)
+    # direction must match the memory kinds
+    assert dv.dv_swap_out(h, 0, d, 0, 0, 2, z, t1, check=False) == dv.DV_ERR_INVALID
+    assert dv.dv_swap_in(d, 0, h, 0, 0, 2, z, t1, check=False) == dv.DV_ERR_INVALID
+    # shapes must agree
+    h2 = dense(H=4, bases=(FAKE + (1 << 33),), mem=dv.DV_MEM_HOST_PINNED)
+    assert dv.dv_swap_out(d, 0, h2, 0, 0, 2, z, t1, check=False) == dv.DV_ERR_INVALID
+    # the host mirror must hold the range
+    hs = dense(S=8, bases=(FAKE + (1 << 33),), mem=dv.DV_MEM_HOST_PINNED)
+    assert dv.dv_swap_out(d, 0, hs, 0, 0, 2, z, t1, check=False) == dv.DV_ERR_RANGE
+    # paged caches are not swapped
+    p = dv.Cache(dv.DV_PAGED, 2, 3, 64, 4, [FAKE], block_size=16, num_blocks=8, max_blocks=4,
+                 block_tables=[FAKE])
+    assert dv.dv_swap_out(p, 0, h, 0, 0, 2, z, t1, check=False) == dv.DV_ERR_UNSUPPORTED
+    # empty ranges are a no-op
+    assert dv.dv_swap_out(d, 0, h, 0, 0, 2, z, z) == dv.DV_OK

@@ -1,0 +1,153 @@
+"""Microbatch swapping between device slots and pinned host mirrors."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2403_01876_amd import dv  # noqa: E402
+from tests import gpu_util as G  # noqa: E402
+
+
+def pinned(nbytes: int, byte: int) -> torch.Tensor:
+    t = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    t.fill_(byte)
+    return t
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_swap_out_in_matches_oracle(oracle_lib, seed):
+    r = np.random.default_rng(500 + seed)
+    L, H, B = int(r.integers(1, 4)), int(r.integers(1, 6)), int(r.integers(1, 9))
+    D, E = int(r.choice([64, 128])), 2
+    S_dev = int(r.integers(8, 300))
+    S_host = int(r.integers(S_dev // 2, S_dev + 50))
+    cap = min(S_dev, S_host)
+    dl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S_dev, elem_bytes=E)
+    hl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S_host, elem_bytes=E)
+    slot_h = synth.fill_bytes(dl.storage_bytes(), seed)
+    slot = G.to_dev(slot_h)
+    host = pinned(hl.storage_bytes(), 0x77)
+    d = dv.Cache(dv.DV_DENSE, L, H, D, B, [slot], max_seq=S_dev)
+    h = dv.Cache(dv.DV_DENSE, L, H, D, B, [host.data_ptr()], max_seq=S_host,
+                 mem=dv.DV_MEM_HOST_PINNED)
+    if seed % 2 == 0:  # uniform ranges: one 2-D copy
+        a = int(r.integers(0, cap))
+        t0 = np.full(B, a, np.int32)
+        t1 = np.full(B, int(r.integers(a, cap + 1)), np.int32)
+    else:
+        t0 = r.integers(0, cap // 2 + 1, size=B).astype(np.int32)
+        t1 = np.minimum(t0 + r.integers(0, cap, size=B), cap).astype(np.int32)
+    l0 = int(r.integers(0, L))
+    l1 = int(r.integers(l0 + 1, L + 1))
+    side = torch.cuda.Stream()
+    dv.dv_swap_out(d, 0, h, 0, l0, l1, t0, t1, side)
+    side.synchronize()
+    exp_host = np.full(hl.storage_bytes(), 0x77, np.uint8)
+    oracle_lib.copy_ranges(dl, slot_h, hl, exp_host, l0, l1, t0, t1)
+    assert host.numpy().tobytes() == exp_host.tobytes()
+    # swap back into a sentinel slot
+    slot2 = G.dev_const(dl.storage_bytes(), 0xA5)
+    d2 = dv.Cache(dv.DV_DENSE, L, H, D, B, [slot2], max_seq=S_dev)
+    dv.dv_swap_in(h, 0, d2, 0, l0, l1, t0, t1, side)
+    side.synchronize()
+    exp_slot = np.full(dl.storage_bytes(), 0xA5, np.uint8)
+    oracle_lib.copy_ranges(hl, exp_host, dl, exp_slot, l0, l1, t0, t1)
+    assert G.host(slot2).tobytes() == exp_slot.tobytes()
+
+
+def test_opt66b_round_robin_swapping(oracle_lib):
+    """Four microbatches through two device slots, two rounds.
+
+    Before microbatch x's step its whole cache has been prefetched into its
+    slot; the step writes one token per layer (emulated by streaming in a
+    generated increment) and packs that increment on the compute stream;
+    after the step only the step's token is swapped out, while the next
+    microbatch is swapped in on another stream.  Device reference caches get
+    the same token writes; at the end every host mirror, swapped back in,
+    equals its reference.
+    """
+    w = synth.make_workload(2)
+    L, H, D, B, S, E = w.layers, w.heads, w.head_dim, w.batch, w.max_seq, w.elem_bytes
+    M = w.microbatches
+    S_host = 1024
+    dl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S, elem_bytes=E)
+    hl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S_host, elem_bytes=E)
+    seeds = [synth.derived_seed(w.seed, 0x100 + x) for x in range(M)]
+    slots = [G.dev_const(dl.storage_bytes(), 0) for _ in range(w.device_slots)]
+    refs = [G.dev_filled(dl.storage_bytes(), seeds[x]) for x in range(M)]
+    hosts = [pinned(hl.storage_bytes(), 0) for _ in range(M)]
+    ds = dv.Cache(dv.DV_DENSE, L, H, D, B, slots, max_seq=S)
+    dr = dv.Cache(dv.DV_DENSE, L, H, D, B, refs, max_seq=S)
+    hh = dv.Cache(dv.DV_DENSE, L, H, D, B, [t.data_ptr() for t in hosts], max_seq=S_host,
+                  mem=dv.DV_MEM_HOST_PINNED)
+    lens = [np.full(B, 1000, np.int32) for _ in range(M)]
+    zero = np.zeros(B, np.int32)
+    compute, s_out, s_in = torch.cuda.current_stream(), torch.cuda.Stream(), torch.cuda.Stream()
+
+    # the prompt caches start on the host
+    for x in range(M):
+        dv.dv_swap_out(dr, x, hh, x, 0, L, zero, lens[x], compute)
+    compute.synchronize()
+    # sampled check of one mirror against the oracle's copy map
+    rng = np.random.default_rng(2)
+    nel = oracle_lib.wire_elems(dl, 0, L, zero, lens[1])
+    widx = rng.integers(0, nel, size=1 << 16)
+    i_dev = oracle_lib.wire_to_storage(dl, 0, L, zero, lens[1], widx)
+    i_host = oracle_lib.wire_to_storage(hl, 0, L, zero, lens[1], widx)
+    got = hosts[1].numpy().view(np.uint16)[i_host]
+    exp = synth.bytes_at(seeds[1], i_dev.astype(np.uint64) * np.uint64(E), E).astype(np.uint16)
+    assert np.array_equal(got, exp)
+
+    inc_n = L * 2 * B * H * D * E
+    assert inc_n == 4718592
+    inc = torch.empty(inc_n, dtype=torch.uint8, device=G.DEV)
+    tok = torch.empty(inc_n, dtype=torch.uint8, device=G.DEV)
+    swapped_in = [torch.cuda.Event() for _ in range(w.device_slots)]
+    slot_free = [torch.cuda.Event() for _ in range(w.device_slots)]
+    for e in slot_free:
+        e.record(compute)
+    # prefetch microbatch 0 into slot 0
+    s_in.wait_event(slot_free[0])
+    dv.dv_swap_in(hh, 0, ds, 0, 0, L, zero, lens[0], s_in)
+    swapped_in[0].record(s_in)
+    steps = 2 * M
+    for k in range(steps):
+        x, slot, nxt = k % M, k % 2, (k + 1) % 2
+        # prefetch the next microbatch into the other slot once its previous
+        # occupant's update has reached the host
+        if k + 1 < steps:
+            s_in.wait_event(slot_free[nxt])
+            xn = (k + 1) % M
+            dv.dv_swap_in(hh, xn, ds, nxt, 0, L, zero, lens[xn], s_in)
+            swapped_in[nxt].record(s_in)
+        # the step itself on the compute stream
+        compute.wait_event(swapped_in[slot])
+        pos = lens[x]
+        synth.device_fill(tok.data_ptr(), inc_n, synth.derived_seed(w.seed, 0x200 + k),
+                          stream=compute.cuda_stream)
+        dv.dv_stream_in(ds, slot, 0, L, pos, pos + 1, tok, inc_n, compute)
+        dv.dv_stream_in(dr, x, 0, L, pos, pos + 1, tok, inc_n, compute)
+        dv.dv_stream_out_token(ds, slot, 0, L, pos, inc, inc_n, compute)
+        done = torch.cuda.Event()
+        done.record(compute)
+        # swap out only the step's update, then free the slot
+        s_out.wait_event(done)
+        dv.dv_swap_out(ds, slot, hh, x, 0, L, pos, pos + 1, s_out)
+        slot_free[slot].record(s_out)
+        lens[x] = pos + 1
+        # the packed increment equals the token just written
+        compute.synchronize()
+        assert torch.equal(inc, tok)
+    torch.cuda.synchronize()
+    # every mirror swapped back in equals its reference on [0, len)
+    for x in range(M):
+        dv.dv_swap_in(hh, x, ds, 0, 0, L, zero, lens[x], compute)
+        compute.synchronize()
+        G.assert_dense_ranges_equal(slots[0], refs[x], L, B, H, S, D, E, 0, L, zero, lens[x])

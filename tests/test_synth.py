@@ -52,3 +52,10 @@ def test_workloads_shapes_and_lengths():
     assert not np.array_equal(w4.block_table_a, w4.block_table_b)
     # deterministic from the seed
     assert np.array_equal(synth.make_workload(4).block_table_a, w4.block_table_a)
+
+
+def test_host_c_fill_equals_numpy_definition():
+    synth.build_host()
+    for n, first in [(1, 0), (7, 3), (4096, 0), (1000, 13), (65536 + 5, 1 << 35)]:
+        assert synth.fill_bytes(n, 99, first).tobytes() == \
+            synth.fill_bytes_numpy(n, 99, first).tobytes()
