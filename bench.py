@@ -48,6 +48,8 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-extras", action="store_true")
+    p.add_argument("--extras", choices=("all", "calib", "none"), default="all",
+                   help="calib: only the known-size copy used to scale counter runs")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--graph", action="store_true",
                    help="replay each step as one captured HIP graph")
@@ -465,6 +467,26 @@ def cpu_baseline():
     }
 
 
+def counted_traffic():
+    """HBM bytes per launch of the bulk pack kernel from the committed counter
+    summary, or None if the kernel sources changed since it was taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "dense_runs_hbm_traffic_opt13b_stage.md")
+    try:
+        text = open(path).read()
+    except OSError:
+        return None
+    m_sha = re.search(r"^kernel_source_sha256: ([0-9a-f]{64})$", text, re.M)
+    m_t = re.search(r"^traffic_bytes_per_launch: (\d+)$", text, re.M)
+    if not (m_sha and m_t):
+        return None
+    h = hashlib.sha256()
+    for f in ("dv_kernels.hip", "dv_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2403_01876_amd", "csrc", f), "rb").read())
+    return int(m_t.group(1)) if h.hexdigest() == m_sha.group(1) else None
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -528,7 +550,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(pack_gbs / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": counted_traffic(),
             "avg_ms": round(r["pack_ms"], 4),
             "bytes_per_launch": 2 * r["P"],
         },
@@ -542,7 +564,10 @@ def main():
         for k, key in (("token_kernel<pack>", "tok_ms"), ("token_kernel<unpack>", "tokin_ms")):
             out["kernels"][k] = {"avg_ms_first_step": round(r[key], 4),
                                  "GBps_2x": round(2 * r["I"] / (r[key] * 1e-3) / 1e9, 1)}
-    if not args.no_extras:
+    extras = "none" if args.no_extras else args.extras
+    if extras == "calib":
+        out["calibration_d2d_copy"] = copy_calibration(torch)
+    if extras == "all":
         log("extras: increments")
         out["increments"] = increments_bench(torch, dv, synth)
         log("extras: bulk workloads")

@@ -222,7 +222,9 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
       a.r = r;
       int64_t tiles = 0;
       for (int i = 0; i < nseq; ++i)
-        if (r.n[i] > 0) tiles += (r.t0[i] + r.n[i] + v.bs - 1) / v.bs - r.t0[i] / v.bs;
+        if (r.n[i] > 0)
+          tiles += ((r.t0[i] + r.n[i] + v.bs - 1) / v.bs - r.t0[i] / v.bs) *
+                   ((v.H + dv::kPagedHeads - 1) / dv::kPagedHeads);
       if (tiles >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
       const hipError_t e = dv::launch_paged(dir, a, (uint32_t)tiles, 2 * nl, st);
       if (e != hipSuccess) return hip_fail(e, "paged kernel launch");

@@ -103,8 +103,16 @@ hipError_t launch_ksplit(int dir, const KsplitArgs& a, uint32_t tiles_per_slab, 
                          hipStream_t s);
 
 // Units each dense-run workgroup moves (tiles are counted on the host with
-// the same constant).
-constexpr int kDenseUnroll = 8;
+// the same constant).  Two 16-byte units per lane (8 KB per workgroup) keeps
+// register use low enough for full occupancy; measured on MI355X against 1,
+// 3, 4, 8 and 16 units per lane on the OPT-13B stage shape.
+constexpr int kDenseUnroll = 2;
 constexpr int kDenseTile = kThreads * kDenseUnroll;
+
+// Heads per paged tile and 16-byte units per lane per pass (tiles are
+// counted on the host with kPagedHeads).  Measured on MI355X against 1, 4
+// and all heads per tile on the LLaMA-2-70B paged shape.
+constexpr int kPagedHeads = 2;
+constexpr int kPagedUnroll = 2;
 
 }  // namespace dv

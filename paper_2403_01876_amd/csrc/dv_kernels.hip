@@ -80,12 +80,13 @@ __global__ void __launch_bounds__(kThreads) dense_runs_kernel(DenseRunArgs a) {
   u32x4* dst = (D == kPack) ? wire : cache;
   const int count = min(kDenseTile, run_b - k * kDenseTile);
 
+  // Loads carry no per-lane guard (a lane past the tile's end re-reads the
+  // tile's last unit), so they issue back to back with a single wait; a
+  // guarded load would make the compiler wait after every one.
   u32x4 v[kDenseUnroll];
 #pragma unroll
-  for (int i = 0; i < kDenseUnroll; ++i) {
-    const int idx = i * kThreads + threadIdx.x;
-    if (idx < count) v[i] = ld_nt(src + idx);
-  }
+  for (int i = 0; i < kDenseUnroll; ++i)
+    v[i] = ld_nt(src + min(i * kThreads + (int)threadIdx.x, count - 1));
 #pragma unroll
   for (int i = 0; i < kDenseUnroll; ++i) {
     const int idx = i * kThreads + threadIdx.x;
@@ -95,33 +96,35 @@ __global__ void __launch_bounds__(kThreads) dense_runs_kernel(DenseRunArgs a) {
 
 // ---------------------------------------------------------------------------
 // Paged blocks: grid (tiles_per_slab, nslabs); a tile is the part of one
-// logical block of one sequence inside its token range, all heads.  For a
-// fixed (slab, block) the pool holds the heads back to back, so a full
-// block is heads*bs*du contiguous units.
+// logical block of one sequence inside its token range, for kPagedHeads
+// heads.  For a fixed (slab, block) the pool holds the heads back to back,
+// so the tile's pool side is one contiguous piece; on the wire side each
+// head's tokens are contiguous.  Two heads of a 16-token, 128-dim block make
+// an 8 KB tile, the size the dense kernel streams best at.
 // ---------------------------------------------------------------------------
-constexpr int kPagedHeadUnroll = 8;
-
 template <int D>
 __global__ void __launch_bounds__(kThreads) paged_kernel(PagedArgs a) {
   const int lane = lane_id();
   const int bs = a.block_size;
-  int n = 0, t0 = 0, nblk = 0;
+  const int ngrp = (a.heads + kPagedHeads - 1) / kPagedHeads;
+  int n = 0, t0 = 0, tiles = 0;
   if (lane < a.nseq) {
     n = a.r.n[lane];
     t0 = a.r.t0[lane];
-    if (n > 0) nblk = (t0 + n + bs - 1) / bs - t0 / bs;
+    if (n > 0) tiles = ((t0 + n + bs - 1) / bs - t0 / bs) * ngrp;
   }
-  const int incl = wave_incl_scan(nblk);
+  const int incl = wave_incl_scan(tiles);
   const int tok_incl = wave_incl_scan(n);
 
   const int tile = blockIdx.x;
   const int b = owner_lane(incl, tile);
-  const int excl_b = __shfl(incl - nblk, b, 64);
+  const int excl_b = __shfl(incl - tiles, b, 64);
   const int n_b = __shfl(n, b, 64);
   const int t0_b = __shfl(t0, b, 64);
   const int p_b = __shfl(tok_incl - n, b, 64);
-
-  const int j = t0_b / bs + (tile - excl_b);
+  const int tj = tile - excl_b;
+  const int grp = tj % ngrp;
+  const int j = t0_b / bs + tj / ngrp;  // logical block
   const int s_lo = max(t0_b, j * bs);
   const int s_hi = min(t0_b + n_b, (j + 1) * bs);
   const int blk = a.bt[(int64_t)(a.b0 + b) * a.max_blocks + j];
@@ -131,31 +134,30 @@ __global__ void __launch_bounds__(kThreads) paged_kernel(PagedArgs a) {
   const int64_t y = blockIdx.y;
   const int64_t slab = a.m.slab0 + y * a.m.slab_step;
   const int64_t wslab = a.m.wslab0 + y * a.m.slab_step;
+  const int h0 = grp * kPagedHeads;
   u32x4* pool = (u32x4*)a.pool + slab * a.s_slab + (int64_t)blk * a.s_blk +
-                (int64_t)(s_lo - j * bs) * a.du;
-  u32x4* wire = (u32x4*)a.wire + wslab * a.m.w_slab + (int64_t)p_b * a.heads * a.du +
-                (int64_t)(s_lo - t0_b) * a.du;
+                (int64_t)h0 * a.s_h + (int64_t)(s_lo - j * bs) * a.du;
   const int64_t w_h = (int64_t)n_b * a.du;  // wire units per head of this sequence
+  u32x4* wire = (u32x4*)a.wire + wslab * a.m.w_slab + (int64_t)p_b * a.heads * a.du +
+                (int64_t)h0 * w_h + (int64_t)(s_lo - t0_b) * a.du;
 
-  for (int h0 = 0; h0 < a.heads; h0 += kPagedHeadUnroll) {
-    for (int e = threadIdx.x; e < run; e += kThreads) {
-      u32x4 v[kPagedHeadUnroll];
+  // Flattened (head, unit) index over the tile; loads unguarded as in the
+  // dense kernel (a lane past the end re-reads the last unit).
+  const int total = min(kPagedHeads, a.heads - h0) * run;
+  for (int base = 0; base < total; base += kPagedUnroll * kThreads) {
+    u32x4 v[kPagedUnroll];
+    int hh[kPagedUnroll], ee[kPagedUnroll];
 #pragma unroll
-      for (int i = 0; i < kPagedHeadUnroll; ++i) {
-        const int h = h0 + i;
-        if (h < a.heads) {
-          const u32x4* src = (D == kPack) ? pool + h * a.s_h + e : wire + h * w_h + e;
-          v[i] = ld_nt(src);
-        }
-      }
+    for (int i = 0; i < kPagedUnroll; ++i) {
+      const int idx = min(base + i * kThreads + (int)threadIdx.x, total - 1);
+      hh[i] = idx / run;
+      ee[i] = idx - hh[i] * run;
+      v[i] = ld_nt((D == kPack) ? pool + hh[i] * a.s_h + ee[i] : wire + hh[i] * w_h + ee[i]);
+    }
 #pragma unroll
-      for (int i = 0; i < kPagedHeadUnroll; ++i) {
-        const int h = h0 + i;
-        if (h < a.heads) {
-          u32x4* dst = (D == kPack) ? wire + h * w_h + e : pool + h * a.s_h + e;
-          st_nt(v[i], dst);
-        }
-      }
+    for (int i = 0; i < kPagedUnroll; ++i) {
+      if (base + i * kThreads + (int)threadIdx.x < total)
+        st_nt(v[i], (D == kPack) ? wire + hh[i] * w_h + ee[i] : pool + hh[i] * a.s_h + ee[i]);
     }
   }
 }
