@@ -9,17 +9,21 @@ prompt lengths uniform 512..1024 from the seed):
   (dense unpack) -> 128 decode-step increments, each packed out of the
   sender and streamed into the receiver.
 
-Inputs are resident in HBM before timing starts.  ``value`` is algorithmic
-bytes per step (every payload byte read once and written once: 2 x payload
-per call) over the step time, in GB/s.  ``roofline`` is the bulk pack kernel
-(the dense-run kernel of the prompt stream-out) timed with HIP events on its
+Inputs are resident in HBM before timing starts.  The step's 258 calls are
+captured once into a HIP graph and the graph is replayed (the decode-step
+increments are launch-bound, 1.6 MB each); the same step issued call by call
+is timed too and reported as ``eager_ms_per_step`` (``--eager`` makes it the
+headline).  ``value`` is algorithmic bytes per step (every payload byte read
+once and written once: 2 x payload per call) over the step time, in GB/s.
+``roofline`` is the bulk pack kernel (the dense-run kernel of the prompt
+stream-out), its duration from HIP events around back-to-back launches on its
 stream.  Further objects report the other kernels, the microbatch swap over
 the host link (OPT-66B stage), the paged gather/scatter (LLaMA-2-70B GQA),
 the full-cache replica and restore (BLOOM-176B shard), and the oracle timed
 on the host cores.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extras]
-                       [--no-cpu-baseline]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--eager]
+                       [--extras all|calib|none] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -51,8 +55,8 @@ def parse():
     p.add_argument("--extras", choices=("all", "calib", "none"), default="all",
                    help="calib: only the known-size copy used to scale counter runs")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--graph", action="store_true",
-                   help="replay each step as one captured HIP graph")
+    p.add_argument("--eager", action="store_true",
+                   help="report the step issued call by call instead of graph-replayed")
     return p.parse_args()
 
 
@@ -87,6 +91,10 @@ def flush_l2(torch, scratch):
 
 
 def main_step_bench(args, torch, dv, synth):
+    """The step on the OPT-13B stage: replayed as one captured HIP graph (the
+    default; the 258 launches of a step are launch-bound otherwise) or issued
+    eagerly call by call (--eager).  Both are timed; ``value`` uses the mode
+    asked for."""
     dev = torch.device("cuda:0")
     w = synth.make_workload(1)
     L, H, D, B, S = w.layers, w.heads, w.head_dim, w.batch, w.max_seq
@@ -101,91 +109,74 @@ def main_step_bench(args, torch, dv, synth):
     P = dv.dv_packed_bytes(cs, 0, L, t0, t1)
     wire = torch.empty(P, dtype=torch.uint8, device=dev)
     pos = [w.step_positions(i) for i in range(w.steps)]
-    I = dv.dv_packed_bytes(cs, 0, L, pos[0], pos[0] + 1)
-    incs = torch.empty(I, dtype=torch.uint8, device=dev)
     ends = [p + 1 for p in pos]
+    I = dv.dv_packed_bytes(cs, 0, L, pos[0], ends[0])
+    incs = torch.empty(I, dtype=torch.uint8, device=dev)
 
-    t_pack = Timer(torch, stream)
-    t_unpack = Timer(torch, stream)
-    t_tok = Timer(torch, stream)
-    t_tokin = Timer(torch, stream)
+    def pack(st):
+        dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, P, st)
 
-    def step(timed: bool):
-        if timed:
-            with t_pack:
-                dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, P, stream)
-            with t_unpack:
-                dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, stream)
-        else:
-            dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, P, stream)
-            dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, stream)
+    def unpack(st):
+        dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, st)
+
+    def step(st):
+        pack(st)
+        unpack(st)
         for i in range(w.steps):
-            if timed and i == 0:
-                with t_tok:
-                    dv.dv_stream_out_token(cs, 0, 0, L, pos[i], incs, I, stream)
-                with t_tokin:
-                    dv.dv_stream_in(cr, 0, 0, L, pos[i], ends[i], incs, I, stream)
-            else:
-                dv.dv_stream_out_token(cs, 0, 0, L, pos[i], incs, I, stream)
-                dv.dv_stream_in(cr, 0, 0, L, pos[i], ends[i], incs, I, stream)
+            dv.dv_stream_out_token(cs, 0, 0, L, pos[i], incs, I, st)
+            dv.dv_stream_in(cr, 0, 0, L, pos[i], ends[i], incs, I, st)
 
-    graph = None
-    if args.graph:
-        s = torch.cuda.Stream()
-        s.wait_stream(stream)
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.stream(s):
-            step(False)  # warm
-            with torch.cuda.graph(graph, stream=s):
-                gs = torch.cuda.current_stream()
-                dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, P, gs)
-                dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, gs)
-                for i in range(w.steps):
-                    dv.dv_stream_out_token(cs, 0, 0, L, pos[i], incs, I, gs)
-                    dv.dv_stream_in(cr, 0, 0, L, pos[i], ends[i], incs, I, gs)
+    def timed(fn, n):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(n):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
 
+    # eager
     for _ in range(args.warmup):
-        if graph is not None:
-            graph.replay()
-        else:
-            step(False)
+        step(stream)
+    eager_ms = timed(lambda: step(stream), args.steps)
+    log(f"eager: {eager_ms:.3f} ms/step")
+    # graph
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            step(torch.cuda.current_stream())
     torch.cuda.synchronize()
-    log(f"warmup done ({args.warmup} steps)")
-    a = torch.cuda.Event(enable_timing=True)
-    b = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    a.record(stream)
-    for _ in range(args.steps):
-        if graph is not None:
-            graph.replay()
-        else:
-            step(True)
-    b.record(stream)
-    torch.cuda.synchronize()
-    ms = a.elapsed_time(b) / args.steps
-    log(f"timed {args.steps} steps: {ms:.3f} ms/step")
+    for _ in range(args.warmup):
+        graph.replay()
+    graph_ms = timed(graph.replay, args.steps)
+    log(f"graph: {graph_ms:.3f} ms/step")
+    ms = eager_ms if args.eager else graph_ms
+
+    # Per-kernel durations: one event pair around back-to-back launches that
+    # follow a leading untimed one, so the queue never drains and the mean is
+    # pure kernel time (an event pair per launch would add its own packets).
+    kern = {}
+    for name, fn in (("pack", pack), ("unpack", unpack)):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        fn(stream)
+        a.record(stream)
+        for _ in range(args.steps):
+            fn(stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        kern[name] = a.elapsed_time(b) / args.steps
     step_bytes = 2 * P * 2 + w.steps * 2 * I * 2
     res = {
-        "ms": ms, "P": P, "I": I, "step_bytes": step_bytes,
-        "value": step_bytes / (ms * 1e-3) / 1e9,
+        "ms": ms, "eager_ms": eager_ms, "graph_ms": graph_ms, "P": P, "I": I,
+        "step_bytes": step_bytes, "value": step_bytes / (ms * 1e-3) / 1e9,
+        "pack_ms": kern["pack"], "unpack_ms": kern["unpack"],
     }
-    if graph is None:
-        res["pack_ms"] = t_pack.mean_ms()
-        res["unpack_ms"] = t_unpack.mean_ms()
-        res["tok_ms"] = t_tok.mean_ms()
-        res["tokin_ms"] = t_tokin.mean_ms()
-    else:
-        # time the bulk kernels separately for the roofline
-        for _ in range(3):
-            with t_pack:
-                dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, P, stream)
-            with t_unpack:
-                dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, stream)
-        torch.cuda.synchronize()
-        res["pack_ms"] = t_pack.mean_ms()
-        res["unpack_ms"] = t_unpack.mean_ms()
-    del sender, recv, wire, incs
+    del sender, recv, wire, incs, graph
     torch.cuda.empty_cache()
     return w, res
 
@@ -255,8 +246,9 @@ def S_of(w):
     return w.max_seq
 
 
-def bulk_bench(torch, dv, synth, idx, reps=10):
-    """Bulk stream-out and stream-in of one workload, timed per call."""
+def bulk_bench(torch, dv, synth, idx, reps=10, ksplit=False):
+    """Bulk stream-out and stream-in of one workload, timed per call (with
+    ``ksplit``, the dense workload stored with the split-key layout)."""
     dev = torch.device("cuda:0")
     w = synth.make_workload(idx)
     L, H, D, B = w.layers, w.heads, w.head_dim, w.batch
@@ -276,8 +268,9 @@ def bulk_bench(torch, dv, synth, idx, reps=10):
         nbytes = w.dense_bytes()
         a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
         r = torch.zeros(nbytes, dtype=torch.uint8, device=dev)
-        ca = dv.Cache(dv.DV_DENSE, L, H, D, B, [a], max_seq=w.max_seq)
-        cr = dv.Cache(dv.DV_DENSE, L, H, D, B, [r], max_seq=w.max_seq)
+        kind = dv.DV_DENSE_KSPLIT if ksplit else dv.DV_DENSE
+        ca = dv.Cache(kind, L, H, D, B, [a], max_seq=w.max_seq)
+        cr = dv.Cache(kind, L, H, D, B, [r], max_seq=w.max_seq)
     synth.device_fill(a.data_ptr(), nbytes, w.data_seed, stream=stream.cuda_stream)
     t0, t1 = w.prompt_ranges()
     P = dv.dv_packed_bytes(ca, 0, L, t0, t1)
@@ -541,7 +534,9 @@ def main():
             "payload_prompt_bytes": r["P"],
             "payload_increment_bytes": r["I"],
             "algorithmic_bytes_per_step": r["step_bytes"],
-            "graph": bool(args.graph),
+            "step_issue": "eager" if args.eager else "hip graph replay",
+            "eager_ms_per_step": round(r["eager_ms"], 4),
+            "graph_ms_per_step": round(r["graph_ms"], 4),
         },
         "roofline": {
             "kernel": "dense_runs_kernel<pack> (prompt stream-out)",
@@ -560,10 +555,6 @@ def main():
                                           "frac_hbm": round(unpack_gbs / HBM_PEAK_GBS, 4)},
         },
     }
-    if "tok_ms" in r:
-        for k, key in (("token_kernel<pack>", "tok_ms"), ("token_kernel<unpack>", "tokin_ms")):
-            out["kernels"][k] = {"avg_ms_first_step": round(r[key], 4),
-                                 "GBps_2x": round(2 * r["I"] / (r[key] * 1e-3) / 1e9, 1)}
     extras = "none" if args.no_extras else args.extras
     if extras == "calib":
         out["calibration_d2d_copy"] = copy_calibration(torch)
@@ -574,6 +565,8 @@ def main():
         for idx in (3, 4):
             wk, res = bulk_bench(torch, dv, synth, idx)
             out.setdefault("bulk", {})[wk.name] = res
+        wk, res = bulk_bench(torch, dv, synth, 1, ksplit=True)
+        out["bulk"][wk.name + " split-key"] = res
         log("extras: swap")
         out["swap"] = swap_bench(torch, dv, synth)
         log("extras: copy calibration")
