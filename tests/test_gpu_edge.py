@@ -1,0 +1,225 @@
+"""Edge cases of the HIP path, each compared with the CPU oracle byte for byte."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2403_01876_amd import dv  # noqa: E402
+from tests import gpu_util as G  # noqa: E402
+
+
+def stream():
+    return torch.cuda.current_stream()
+
+
+def dense_roundtrip(orc, L, H, D, B, S, E, l0, l1, t0, t1, seed=0, kind=dv.DV_DENSE):
+    okind = {dv.DV_DENSE: oracle.DENSE, dv.DV_DENSE_KSPLIT: oracle.KSPLIT}[kind]
+    lay = oracle.Layout(okind, L, H, D, B, seq_cap=S, elem_bytes=E)
+    host = synth.fill_bytes(lay.storage_bytes(), seed)
+    cache = G.to_dev(host)
+    c = dv.Cache(kind, L, H, D, B, [cache], max_seq=S, elem_bytes=E)
+    exp = orc.pack(lay, host, l0, l1, t0, t1)
+    wire = G.dev_const(exp.nbytes + 32, 0x5C)
+    n = dv.dv_stream_out_prompt(c, 0, l0, l1, t0, t1, wire, exp.nbytes, stream())
+    recv = G.dev_const(lay.storage_bytes(), 0xA5)
+    r = dv.Cache(kind, L, H, D, B, [recv], max_seq=S, elem_bytes=E)
+    if n:
+        dv.dv_stream_in(r, 0, l0, l1, t0, t1, wire, n, stream())
+    torch.cuda.synchronize()
+    w = G.host(wire)
+    assert n == exp.nbytes and w[:n].tobytes() == exp.tobytes() and (w[n:] == 0x5C).all()
+    exp_recv = np.full(lay.storage_bytes(), 0xA5, np.uint8)
+    orc.unpack(lay, exp_recv, l0, l1, t0, t1, exp)
+    assert G.host(recv)[: lay.storage_bytes()].tobytes() == exp_recv.tobytes()
+
+
+def test_one_unit_per_token(oracle_lib):
+    """head_dim * elem_bytes == 16: one 16-byte unit per token."""
+    B = 5
+    t0 = np.array([0, 3, 0, 7, 2], np.int32)
+    t1 = np.array([9, 3, 1, 31, 30], np.int32)
+    dense_roundtrip(oracle_lib, 2, 3, 8, B, 31, 2, 0, 2, t0, t1)
+    dense_roundtrip(oracle_lib, 2, 3, 8, B, 31, 2, 0, 2, t0, t1, kind=dv.DV_DENSE_KSPLIT)
+    dense_roundtrip(oracle_lib, 1, 2, 16, B, 31, 1, 0, 1, t0, t1)
+
+
+def test_many_heads_and_long_runs(oracle_lib):
+    """128 heads; runs of 3000 tokens span many tiles with a ragged tail."""
+    B = 2
+    t0 = np.array([0, 5], np.int32)
+    t1 = np.array([3000, 2999], np.int32)
+    dense_roundtrip(oracle_lib, 1, 128, 128, B, 3001, 2, 0, 1, t0, t1)
+
+
+def test_two_hundred_sequences_with_an_empty_group(oracle_lib):
+    """Sequences 64..127 stream nothing: their launch is skipped, later groups
+    still land at the right wire offsets."""
+    B = 200
+    r = np.random.default_rng(3)
+    t0 = r.integers(0, 20, size=B).astype(np.int32)
+    t1 = (t0 + r.integers(0, 20, size=B)).astype(np.int32)
+    t1[64:128] = t0[64:128]
+    dense_roundtrip(oracle_lib, 2, 2, 64, B, 40, 2, 0, 2, t0, t1)
+    # and single tokens with the same empty group
+    p = r.integers(0, 40, size=B).astype(np.int32)
+    e = (p + 1).astype(np.int32)
+    e[64:128] = p[64:128]
+    dense_roundtrip(oracle_lib, 2, 2, 64, B, 40, 2, 1, 2, p, e)
+
+
+def test_ranges_at_capacity_end(oracle_lib):
+    S = 77
+    t0 = np.array([76, 0, 77, 40], np.int32)
+    t1 = np.array([77, 77, 77, 77], np.int32)
+    dense_roundtrip(oracle_lib, 3, 4, 64, 4, S, 2, 1, 3, t0, t1)
+    dense_roundtrip(oracle_lib, 3, 4, 64, 4, S, 2, 1, 3, t0, t1, kind=dv.DV_DENSE_KSPLIT)
+
+
+def test_head_dim_512(oracle_lib):
+    """64 units per token (split key is limited to 32 and rejects it)."""
+    t0 = np.array([0, 1], np.int32)
+    t1 = np.array([33, 2], np.int32)
+    dense_roundtrip(oracle_lib, 1, 2, 512, 2, 40, 2, 0, 1, t0, t1)
+    cache, dst = G.dev_const(1 << 20, 0), G.dev_const(1 << 20, 0)
+    lay = dv.Cache(dv.DV_DENSE_KSPLIT, 1, 2, 512, 2, [cache], max_seq=40)
+    rc, _ = dv.dv_stream_out_prompt(lay, 0, 0, 1, t0, t1, dst, 1 << 20, check=False)
+    assert rc == dv.DV_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("bs", [1, 64])
+def test_paged_block_sizes(oracle_lib, bs):
+    L, H, D, B, E = 2, 3, 128, 4, 2
+    lens = [130, 0, 1, 64]
+    maxb = max((n + bs - 1) // bs for n in lens) + 1
+    bt, nb = synth.make_paged_tables(bs, lens, bs, maxb)
+    lay = oracle.Layout(oracle.PAGED, L, H, D, B, elem_bytes=E, block_size=bs, num_blocks=nb,
+                        block_table=bt)
+    host = synth.fill_bytes(lay.storage_bytes(), bs)
+    pool = G.to_dev(host)
+    btd = G.to_dev(bt)
+    c = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool], block_size=bs, num_blocks=nb,
+                 max_blocks=maxb, block_tables=[btd])
+    t0 = np.array([3, 0, 0, 10], np.int32)
+    t1 = np.array([130, 0, 1, 64], np.int32)
+    exp = oracle_lib.pack(lay, host, 0, L, t0, t1)
+    wire = G.dev_const(exp.nbytes, 0)
+    dv.dv_stream_out_prompt(c, 0, 0, L, t0, t1, wire, exp.nbytes, stream())
+    torch.cuda.synchronize()
+    assert G.host(wire).tobytes() == exp.tobytes()
+
+
+def test_paged_unmapped_entries_are_skipped(oracle_lib):
+    """Table entries outside [0, num_blocks) inside the ranges: the kernels
+    skip those tokens -- their wire bytes stay unwritten on pack and the pool
+    is untouched on unpack -- and every other token is exact.
+
+    Expected values come from the oracle over a pool with one extra block per
+    (layer, K|V) slab that the invalid entries are pointed at: filled with the
+    wire sentinel for pack, and dropped again after unpack."""
+    L, H, D, B, E, bs = 2, 2, 64, 3, 2, 4
+    bt = np.array([[0, 1, 2], [3, -1, 4], [5, 99, 6]], np.int32)
+    nb = 7
+    blk = H * bs * D * E  # bytes per block per slab
+    bad = (bt < 0) | (bt >= nb)
+    bt_x = np.where(bad, nb, bt).astype(np.int32)
+    ext = oracle.Layout(oracle.PAGED, L, H, D, B, elem_bytes=E, block_size=bs,
+                        num_blocks=nb + 1, block_table=bt_x)
+
+    def with_extra(pool_real, fill):
+        x = pool_real.reshape(L * 2, nb * blk)
+        pad = np.full((L * 2, blk), fill, np.uint8)
+        return np.concatenate([x, pad], axis=1).reshape(-1)
+
+    def drop_extra(pool_ext):
+        return pool_ext.reshape(L * 2, (nb + 1) * blk)[:, : nb * blk].reshape(-1)
+
+    host = synth.fill_bytes(L * 2 * nb * blk, 11)
+    pool = G.to_dev(host)
+    btd = G.to_dev(bt)
+    c = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool], block_size=bs, num_blocks=nb, max_blocks=3,
+                 block_tables=[btd])
+    for single in (False, True):
+        if single:
+            t0 = np.array([5, 5, 5], np.int32)  # logical block 1 of each sequence
+            t1 = t0 + 1
+        else:
+            t0 = np.array([0, 1, 2], np.int32)
+            t1 = np.array([12, 9, 11], np.int32)
+        n = dv.dv_packed_bytes(c, 0, L, t0, t1)
+        wire = G.dev_const(n, 0x5C)
+        if single:
+            dv.dv_stream_out_token(c, 0, 0, L, t0, wire, n, stream())
+        else:
+            dv.dv_stream_out_prompt(c, 0, 0, L, t0, t1, wire, n, stream())
+        torch.cuda.synchronize()
+        exp = oracle_lib.pack(ext, with_extra(host, 0x5C), 0, L, t0, t1)
+        assert G.host(wire).tobytes() == exp.tobytes()
+        # unpack a generated wire into a sentinel pool
+        wh = synth.fill_bytes(n, 21)
+        recv = G.dev_const(L * 2 * nb * blk, 0xA5)
+        rc = dv.Cache(dv.DV_PAGED, L, H, D, B, [recv], block_size=bs, num_blocks=nb,
+                      max_blocks=3, block_tables=[btd])
+        dv.dv_stream_in(rc, 0, 0, L, t0, t1, G.to_dev(wh), n, stream())
+        torch.cuda.synchronize()
+        exp_pool = with_extra(np.full(L * 2 * nb * blk, 0xA5, np.uint8), 0xA5)
+        oracle_lib.unpack(ext, exp_pool, 0, L, t0, t1, wh)
+        assert G.host(recv).tobytes() == drop_extra(exp_pool).tobytes()
+
+
+def test_graph_replay_matches_eager(oracle_lib):
+    """A captured step replayed several times, with eager work and syncs in
+    between, gives the eager result every time."""
+    w = synth.make_workload(0)
+    L, H, D, B, S = w.layers, w.heads, w.head_dim, w.batch, w.max_seq
+    lay = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S)
+    host = synth.fill_bytes(lay.storage_bytes(), 5)
+    src = G.to_dev(host)
+    cs = dv.Cache(dv.DV_DENSE, L, H, D, B, [src], max_seq=S)
+    recv = G.dev_const(lay.storage_bytes(), 0)
+    cr = dv.Cache(dv.DV_DENSE, L, H, D, B, [recv], max_seq=S)
+    t0, t1 = w.prompt_ranges()
+    P = dv.dv_packed_bytes(cs, 0, L, t0, t1)
+    wire = G.dev_const(P, 0)
+    inc = G.dev_const(4096, 0)
+
+    def step(st):
+        dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, P, st)
+        dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, st)
+        for i in range(w.steps):
+            p = w.step_positions(i)
+            dv.dv_stream_out_token(cs, 0, 0, L, p, inc, 4096, st)
+            dv.dv_stream_in(cr, 0, 0, L, p, p + 1, inc, 4096, st)
+
+    step(stream())
+    torch.cuda.synchronize()
+    eager_recv, eager_wire, eager_inc = recv.clone(), wire.clone(), inc.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            step(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    for rep in range(4):
+        recv.fill_(rep + 1)
+        wire.fill_(0x11 * rep)
+        inc.fill_(0x22)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        exp = np.full(lay.storage_bytes(), rep + 1, np.uint8)
+        oracle_lib.unpack(lay, exp, 0, L, t0, t1, oracle_lib.pack(lay, host, 0, L, t0, t1))
+        for i in range(w.steps):
+            p = w.step_positions(i)
+            oracle_lib.unpack(lay, exp, 0, L, p, p + 1,
+                              oracle_lib.pack(lay, host, 0, L, p, p + 1))
+        assert G.host(recv).tobytes() == exp.tobytes(), rep
+        assert torch.equal(wire, eager_wire) and torch.equal(inc, eager_inc), rep
+    del eager_recv
