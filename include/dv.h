@@ -163,10 +163,14 @@ int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const 
  * logical coordinates; all other host bytes are left as they were.  Both
  * caches must be DV_DENSE with equal num_layers, num_heads, head_dim, batch
  * and elem_bytes (their max_seq may differ); `dev` must be DV_MEM_DEVICE and
- * `host` DV_MEM_HOST_PINNED (allocated with hipHostMalloc).  The copy runs
- * on the DMA engines (hipMemcpy2DAsync over the token rows) on `stream`,
- * so it overlaps kernels on other streams.  Swapping a whole microbatch
- * passes its valid lengths; the step-t update passes t0 = t, t1 = t + 1.
+ * `host` DV_MEM_HOST_PINNED (allocated with hipHostMalloc, which kernels can
+ * address).  Rows of 64 KB or more (one sequence's tokens of one head) move
+ * on the DMA engines (hipMemcpy2DAsync over the token rows) on `stream`, so
+ * they overlap kernels on other streams; narrower rows -- a decode step's
+ * update is one 256-byte row per (layer, K|V, sequence, head) -- are copied
+ * by one kernel on `stream` that writes the pinned mirror directly.
+ * Swapping a whole microbatch passes its valid lengths; the step-t update
+ * passes t0 = t, t1 = t + 1.
  * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_UNSUPPORTED, DV_ERR_HIP. */
 int dv_swap_out(const dv_cache* dev, int32_t slot, const dv_cache* host, int32_t host_mb,
                 int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1, void* stream);

@@ -89,6 +89,20 @@ struct KsplitArgs {
   int32_t pad;
   SeqRanges r;
 };
+// Cache-to-cache copy of the same logical positions between two dense
+// caches (device slot <-> pinned host mirror) for narrow rows.
+struct CopyArgs {
+  void* src;
+  void* dst;
+  int64_t s_slab, s_b, s_h;  // source strides (units); token stride du
+  int64_t d_slab, d_b, d_h;  // destination strides (units)
+  int32_t slab0;             // grid row y copies slab slab0 + y
+  int32_t du, heads, nseq, b0;
+  int32_t pad;
+  SeqRanges r;
+};
+constexpr int kCopyUnroll = 2;
+
 constexpr int kKsplitTile = 64;
 constexpr int kKsplitMaxDu = 32;
 
@@ -101,6 +115,7 @@ hipError_t launch_token(int dir, const TokenArgs& a, uint32_t units_per_slab, ui
                         hipStream_t s);
 hipError_t launch_ksplit(int dir, const KsplitArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,
                          hipStream_t s);
+hipError_t launch_copy(const CopyArgs& a, uint32_t units_per_slab, uint32_t nslabs, hipStream_t s);
 
 // Units each dense-run workgroup moves (tiles are counted on the host with
 // the same constant).  Two 16-byte units per lane (8 KB per workgroup) keeps

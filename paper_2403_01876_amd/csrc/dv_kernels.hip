@@ -298,6 +298,56 @@ __global__ void __launch_bounds__(kThreads) ksplit_kernel(KsplitArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Cache-to-cache copy: grid (ceil(units_per_slab / (256 * kCopyUnroll)),
+// nslabs).  Unit u of a slab is the u-th 16-byte unit of the ranges taken
+// in (sequence, head, token, unit) order, i.e. the wire order, but it moves
+// straight from the source cache to the same logical place in the
+// destination cache.  Used for swaps whose rows are too narrow for DMA to
+// run efficiently (a decode step's one-token update is 256-byte rows); on
+// pinned host memory each lane's store or load crosses the host link.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(kThreads) copy_kernel(CopyArgs a) {
+  __shared__ int s_incl[kSeqPerLaunch];
+  const int lane = lane_id();
+  if (threadIdx.x < 64) {
+    const int n = lane < a.nseq ? a.r.n[lane] : 0;
+    s_incl[lane] = wave_incl_scan(n * a.heads * a.du);
+  }
+  __syncthreads();
+  const int total = s_incl[kSeqPerLaunch - 1];
+  const int64_t slab = a.slab0 + (int64_t)blockIdx.y;
+  int64_t so[kCopyUnroll], dst_off[kCopyUnroll];
+  bool ok[kCopyUnroll];
+#pragma unroll
+  for (int i = 0; i < kCopyUnroll; ++i) {
+    const int u0 = (blockIdx.x * kCopyUnroll + i) * kThreads + threadIdx.x;
+    ok[i] = u0 < total;
+    const int u = min(u0, total - 1);
+    // sequence: first lane whose inclusive prefix exceeds u
+    int lo = 0, hi = kSeqPerLaunch - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (s_incl[mid] > u) hi = mid; else lo = mid + 1;
+    }
+    const int b = lo;
+    const int run = a.r.n[b] * a.du;
+    const int rem = u - (s_incl[b] - run * a.heads);
+    const int h = rem / run;
+    const int e = rem - h * run + a.r.t0[b] * a.du;
+    so[i] = slab * a.s_slab + (int64_t)(a.b0 + b) * a.s_b + (int64_t)h * a.s_h + e;
+    dst_off[i] = slab * a.d_slab + (int64_t)(a.b0 + b) * a.d_b + (int64_t)h * a.d_h + e;
+  }
+  const u32x4* src = (const u32x4*)a.src;
+  u32x4* dst = (u32x4*)a.dst;
+  u32x4 v[kCopyUnroll];
+#pragma unroll
+  for (int i = 0; i < kCopyUnroll; ++i) v[i] = ld_nt(src + so[i]);
+#pragma unroll
+  for (int i = 0; i < kCopyUnroll; ++i)
+    if (ok[i]) st_nt(v[i], dst + dst_off[i]);
+}
+
 }  // namespace
 
 namespace {
@@ -339,6 +389,12 @@ hipError_t launch_ksplit(int dir, const KsplitArgs& a, uint32_t tiles_per_slab, 
   const void* fn =
       dir == kPack ? (const void*)&ksplit_kernel<kPack> : (const void*)&ksplit_kernel<kUnpack>;
   return launch(fn, dim3(tiles_per_slab, nslabs), a, s);
+}
+
+hipError_t launch_copy(const CopyArgs& a, uint32_t units_per_slab, uint32_t nslabs,
+                       hipStream_t s) {
+  const uint32_t per = kThreads * kCopyUnroll;
+  return launch((const void*)&copy_kernel, dim3((units_per_slab + per - 1) / per, nslabs), a, s);
 }
 
 }  // namespace dv

@@ -62,6 +62,55 @@ def test_swap_out_in_matches_oracle(oracle_lib, seed):
     assert G.host(slot2).tobytes() == exp_slot.tobytes()
 
 
+@pytest.mark.parametrize("case", ["delta-uniform", "delta-ragged", "wide-uniform",
+                                  "wide-ragged", "mixed"])
+def test_swap_engines_match_oracle(oracle_lib, case):
+    """Both engines: narrow rows (copy kernel) and rows of 64 KB or more (DMA)."""
+    L, H, D, B, E = 2, 3, 128, 5, 2
+    S_dev, S_host = 600, 520
+    r = np.random.default_rng(hash(case) % 1000)
+    if case == "delta-uniform":
+        t0 = np.full(B, 300, np.int32)
+        t1 = t0 + 1
+    elif case == "delta-ragged":
+        t0 = r.integers(0, 519, size=B).astype(np.int32)
+        t1 = t0 + 1
+        t1[2] = t0[2]  # an inactive sequence
+    elif case == "wide-uniform":
+        t0 = np.zeros(B, np.int32)
+        t1 = np.full(B, 500, np.int32)  # 128000-byte rows
+    elif case == "wide-ragged":
+        t0 = r.integers(0, 100, size=B).astype(np.int32)
+        t1 = (t0 + 256 + r.integers(0, 160, size=B)).astype(np.int32)
+    else:  # one wide row makes the whole call DMA; others narrow or empty
+        t0 = np.array([0, 5, 7, 0, 100], np.int32)
+        t1 = np.array([400, 6, 7, 3, 101], np.int32)
+    dl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S_dev, elem_bytes=E)
+    hl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S_host, elem_bytes=E)
+    slot_h = synth.fill_bytes(dl.storage_bytes(), 3)
+    slot = G.to_dev(slot_h)
+    host = pinned(hl.storage_bytes(), 0x77)
+    d = dv.Cache(dv.DV_DENSE, L, H, D, B, [slot], max_seq=S_dev)
+    h = dv.Cache(dv.DV_DENSE, L, H, D, B, [host.data_ptr()], max_seq=S_host,
+                 mem=dv.DV_MEM_HOST_PINNED)
+    side = torch.cuda.Stream()
+    dv.dv_swap_out(d, 0, h, 0, 0, L, t0, t1, side)
+    side.synchronize()
+    exp_host = np.full(hl.storage_bytes(), 0x77, np.uint8)
+    oracle_lib.copy_ranges(dl, slot_h, hl, exp_host, 0, L, t0, t1)
+    assert host.numpy().tobytes() == exp_host.tobytes()
+    # swap a different host content back in
+    host_h = synth.fill_bytes(hl.storage_bytes(), 4)
+    host.copy_(torch.from_numpy(host_h))
+    slot2 = G.dev_const(dl.storage_bytes(), 0xA5)
+    d2 = dv.Cache(dv.DV_DENSE, L, H, D, B, [slot2], max_seq=S_dev)
+    dv.dv_swap_in(h, 0, d2, 0, 0, L, t0, t1, side)
+    side.synchronize()
+    exp_slot = np.full(dl.storage_bytes(), 0xA5, np.uint8)
+    oracle_lib.copy_ranges(hl, host_h, dl, exp_slot, 0, L, t0, t1)
+    assert G.host(slot2).tobytes() == exp_slot.tobytes()
+
+
 def test_opt66b_round_robin_swapping(oracle_lib):
     """Four microbatches through two device slots, two rounds.
 
