@@ -37,6 +37,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+# HIP multiplexes streams onto GPU_MAX_HW_QUEUES hardware queues (4 by
+# default) and two streams sharing one execute in order.  This process
+# creates many streams (torch's pool, graph capture, the swap scheduler's
+# two), and with 4 queues the scheduler's input stream can land on the
+# compute stream's queue, which serialises every swap-in with the step it
+# should hide behind.  8 queues keep them apart.  Set before HIP starts.
+os.environ.setdefault("GPU_MAX_HW_QUEUES", "8")
+
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 PCIE_PEAK_GBS = 63.0        # PCIe Gen5 x16 per direction after 128b/130b encoding
 METRIC = "KV pack/scatter GB/s and % of HBM peak; swap GB/s vs host-link peak (1 GPU)"
@@ -379,6 +387,97 @@ def swap_bench(torch, dv, synth, reps=3):
     return res
 
 
+def swap_protocol_bench(torch, dv, synth, swap_in_gbs):
+    """The paper's microbatch swapping protocol on the OPT-66B stage through
+    the swap scheduler: 4 host microbatches, 2 device slots, 2 rounds.  Each
+    step prefetches the next microbatch, writes one token per layer, runs an
+    emulated decode step (a spin kernel, its length measured with events),
+    packs the increment and swaps out only the step's update.  Swap-ins
+    share the one host link, so the steady-state period should be the
+    longer of the step and one swap-in (App. E's max(t, transf_i)); the
+    App. E break-even step time for 128 generated tokens is reported too."""
+    from paper_2403_01876_amd import swap_model as SM
+    dev = torch.device("cuda:0")
+    w = synth.make_workload(2)
+    L, H, D, B, S = w.layers, w.heads, w.head_dim, w.batch, w.max_seq
+    M, S_host = w.microbatches, 1024
+    compute = torch.cuda.current_stream()
+    slots = [torch.empty(w.dense_bytes(), dtype=torch.uint8, device=dev) for _ in range(2)]
+    synth.device_fill(slots[0].data_ptr(), w.dense_bytes(), w.data_seed,
+                      stream=compute.cuda_stream)
+    hosts = [torch.empty(w.dense_bytes(S_host), dtype=torch.uint8, pin_memory=True)
+             for _ in range(M)]
+    ds = dv.Cache(dv.DV_DENSE, L, H, D, B, slots, max_seq=S)
+    hh = dv.Cache(dv.DV_DENSE, L, H, D, B, [h.data_ptr() for h in hosts], max_seq=S_host,
+                  mem=dv.DV_MEM_HOST_PINNED)
+    zero = np.zeros(B, np.int32)
+    for x in range(M):
+        dv.dv_swap_out(ds, 0, hh, x, 0, L, zero, w.lens.astype(np.int32), compute)
+    I = dv.dv_packed_bytes(ds, 0, L, zero, np.ones(B, np.int32))
+    tok = torch.empty(I, dtype=torch.uint8, device=dev)
+    inc = torch.empty(I, dtype=torch.uint8, device=dev)
+    synth.device_fill(tok.data_ptr(), I, 5, stream=compute.cuda_stream)
+    torch.cuda.synchronize()
+    # spin-kernel calibration: cycles per ms
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(compute)
+    torch.cuda._sleep(10_000_000)
+    b.record(compute)
+    torch.cuda.synchronize()
+    cyc_per_ms = 10_000_000 / a.elapsed_time(b)
+    res = {"microbatches": M, "slots": 2, "steps": 2 * M, "increment_bytes": I}
+    kv_token = L * 2 * H * D * w.elem_bytes
+    bw = swap_in_gbs * 1e9
+    runs = []
+    transf_ms = SM.transfer_time(int(w.lens[0]), B, kv_token, bw) * 1e3
+    for t_ms in (0.0, 40.0, 100.0):
+        lens = [w.lens.astype(np.int32).copy() for _ in range(M)]
+        sw = dv.Swapper(ds, hh)
+        steps = 2 * M
+        sw.prefetch(0, lens[0])
+        torch.cuda.synchronize()
+        marks = []
+        for k in range(steps):
+            x = k % M
+            if k + 1 < steps:
+                sw.prefetch((k + 1) % M, lens[(k + 1) % M])
+            slot = sw.begin_step(x, compute)
+            c0 = torch.cuda.Event(enable_timing=True)
+            c1 = torch.cuda.Event(enable_timing=True)
+            c0.record(compute)
+            pos = lens[x]
+            dv.dv_stream_in(ds, slot, 0, L, pos, pos + 1, tok, I, compute)
+            if t_ms > 0:
+                torch.cuda._sleep(int(t_ms * cyc_per_ms))
+            dv.dv_stream_out_token(ds, slot, 0, L, pos, inc, I, compute)
+            c1.record(compute)
+            sw.end_step(x, pos, pos + 1, compute)
+            lens[x] = pos + 1
+            marks.append((c0, c1))
+        sw.sync()
+        torch.cuda.synchronize()
+        sw.close()
+        if os.environ.get("DV_BENCH_TIMELINE"):
+            for k, (c0, c1) in enumerate(marks):
+                log(f"  t={t_ms} step {k}: start {marks[0][0].elapsed_time(c0):9.2f} ms, "
+                    f"end {marks[0][0].elapsed_time(c1):9.2f} ms")
+        compute_ms = sum(c0.elapsed_time(c1) for c0, c1 in marks) / steps
+        # steady-state period: between the ends of consecutive steps
+        period = marks[0][1].elapsed_time(marks[-1][1]) / (steps - 1)
+        runs.append({"emulated_step_ms": round(compute_ms, 3),
+                     "measured_period_ms": round(period, 3),
+                     "model_period_ms": round(max(compute_ms, transf_ms), 3)})
+    res["swap_in_ms_model"] = round(transf_ms, 3)
+    res["runs"] = runs
+    res["swap_in_GBps_used"] = swap_in_gbs
+    res["breakeven_step_ms_128_tokens"] = round(
+        SM.breakeven_step_time(128, int(w.lens[0]), B, kv_token, bw) * 1e3, 3)
+    del slots, hosts, tok, inc
+    torch.cuda.empty_cache()
+    return res
+
+
 def read_link():
     """PCIe link speed/width of the GPU from sysfs (best effort)."""
     import glob
@@ -569,6 +668,9 @@ def main():
         out["bulk"][wk.name + " split-key"] = res
         log("extras: swap")
         out["swap"] = swap_bench(torch, dv, synth)
+        log("extras: swap protocol")
+        out["swap_protocol"] = swap_protocol_bench(torch, dv, synth,
+                                                   out["swap"]["swap_in"]["GBps"])
         log("extras: copy calibration")
         out["calibration_d2d_copy"] = copy_calibration(torch)
     if not args.no_cpu_baseline:

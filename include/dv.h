@@ -180,6 +180,49 @@ int dv_swap_out(const dv_cache* dev, int32_t slot, const dv_cache* host, int32_t
 int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev, int32_t slot,
                int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Microbatch swap scheduler (Sec. 4.2.2, Figure "swapping").  The caches of
+ * all D microbatches live in pinned host memory (`host`, num_mb = D); two
+ * device slots (`dev_slots`, the first two mb_base entries) hold the
+ * microbatch being processed and the next one.  Per step of microbatch x:
+ *   dv_swapper_prefetch(x+1, len)      swap-in of x+1 into the other slot on
+ *                                      the scheduler's input stream, once that
+ *                                      slot's previous occupant has been
+ *                                      swapped out;
+ *   dv_swapper_begin_step(x, stream)   makes `stream` wait until x is in its
+ *                                      slot; returns the slot for the step;
+ *   ... the step writes the slot on `stream` ...
+ *   dv_swapper_end_step(x, stream, t0, t1)
+ *                                      after the work queued on `stream`, swap
+ *                                      out the part the step updated (tokens
+ *                                      [t0[b], t1[b]), e.g. the one new token)
+ *                                      on the scheduler's output stream.
+ * Slots are dealt alternately in prefetch order.  Ordering is by HIP events
+ * only; no call blocks the host except dv_swapper_sync and destroy.
+ * create allocates two streams and five events (the only allocations);
+ * the descriptors' base arrays are copied.  Overlap needs the scheduler's
+ * streams on hardware queues of their own: HIP maps streams onto
+ * GPU_MAX_HW_QUEUES hardware queues (4 by default) and streams sharing a
+ * queue execute in order, so a process with many streams should raise it
+ * (measured on MI355X: with 4 queues and torch's stream pool the swap-in
+ * and the step serialised; with 8 the swap-in hid behind the step).  Both caches DV_DENSE with equal
+ * shapes (capacities may differ), dev in DV_MEM_DEVICE, host in
+ * DV_MEM_HOST_PINNED.  One scheduler per host thread.
+ * Errors: DV_ERR_INVALID (bad arguments; prefetch into a slot whose
+ * occupant's step has not ended), DV_ERR_RANGE (microbatch outside `host`;
+ * begin/end of a microbatch not prefetched), DV_ERR_UNSUPPORTED, DV_ERR_HIP,
+ * plus those of dv_swap_in / dv_swap_out. */
+typedef struct dv_swapper dv_swapper;
+int dv_swapper_create(const dv_cache* dev_slots, const dv_cache* host, dv_swapper** out);
+int dv_swapper_prefetch(dv_swapper* s, int32_t mb, const int32_t* len);
+int dv_swapper_begin_step(dv_swapper* s, int32_t mb, void* compute_stream, int32_t* slot_out);
+int dv_swapper_end_step(dv_swapper* s, int32_t mb, void* compute_stream, const int32_t* t0,
+                        const int32_t* t1);
+/* Waits for all swaps queued so far. */
+int dv_swapper_sync(dv_swapper* s);
+/* Waits for queued swaps, then frees the scheduler's streams and events. */
+int dv_swapper_destroy(dv_swapper* s);
+
 /* Static text for a dv_status value. */
 const char* dv_status_string(int status);
 

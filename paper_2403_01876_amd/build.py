@@ -24,7 +24,8 @@ def _run(cmd):
 
 
 def build_libdv(out: str = LIBDV) -> str:
-    srcs = [os.path.join(PKG, "csrc", "dv_kernels.hip"), os.path.join(PKG, "csrc", "dv_api.cpp")]
+    srcs = [os.path.join(PKG, "csrc", f) for f in ("dv_kernels.hip", "dv_api.cpp",
+                                                    "dv_swapper.cpp")]
     tmp = out + ".tmp"
     _run([HIPCC, *HIP_FLAGS, "-x", "hip", *srcs, "-o", tmp])
     os.replace(tmp, out)

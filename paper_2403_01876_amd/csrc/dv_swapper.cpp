@@ -1,0 +1,164 @@
+// Microbatch swap scheduler: the round-robin protocol of the paper's
+// microbatch swapping (Sec. 4.2.2, Figure "swapping").  All microbatches'
+// caches live in pinned host memory; two device slots hold the microbatch
+// being processed and the next one.  Before microbatch x's step the
+// scheduler has prefetched x into a slot (swap-in on its own stream); after
+// the step it swaps out only the part the step updated (swap-out on a second
+// stream), which also frees the slot for the microbatch after next.  Data
+// movement goes through dv_swap_in / dv_swap_out; this file only orders it
+// with HIP events.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "../../include/dv.h"
+
+struct dv_swapper {
+  dv_cache dev, host;
+  std::vector<void*> dev_base, host_base;
+  hipStream_t s_in = nullptr, s_out = nullptr;
+  hipEvent_t resident[2] = {nullptr, nullptr};  // swap-in into the slot done
+  hipEvent_t freed[2] = {nullptr, nullptr};     // slot's last occupant swapped out
+  hipEvent_t step_done = nullptr;
+  int next_slot = 0;
+  std::vector<int> slot_of;  // per host microbatch: slot it is in, or -1
+  int occupant[2] = {-1, -1};
+  // A slot may be refilled only after its occupant's step has ended (its
+  // update is then queued for swap-out and `freed` orders the refill).
+  bool done[2] = {true, true};
+};
+
+namespace {
+
+int hip_ok(hipError_t e) { return e == hipSuccess ? DV_OK : DV_ERR_HIP; }
+
+void release(dv_swapper* s) {
+  if (s->s_in) (void)hipStreamSynchronize(s->s_in);
+  if (s->s_out) (void)hipStreamSynchronize(s->s_out);
+  for (int i = 0; i < 2; ++i) {
+    if (s->resident[i]) (void)hipEventDestroy(s->resident[i]);
+    if (s->freed[i]) (void)hipEventDestroy(s->freed[i]);
+  }
+  if (s->step_done) (void)hipEventDestroy(s->step_done);
+  if (s->s_in) (void)hipStreamDestroy(s->s_in);
+  if (s->s_out) (void)hipStreamDestroy(s->s_out);
+  delete s;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dv_swapper_create(const dv_cache* dev_slots, const dv_cache* host, dv_swapper** out) {
+  if (!dev_slots || !host || !out || !dev_slots->mb_base || !host->mb_base) return DV_ERR_INVALID;
+  if (dev_slots->num_mb < 2 || host->num_mb < 1) return DV_ERR_INVALID;
+  if (dev_slots->kind != DV_DENSE || host->kind != DV_DENSE) return DV_ERR_UNSUPPORTED;
+  if (dev_slots->mem != DV_MEM_DEVICE || host->mem != DV_MEM_HOST_PINNED) return DV_ERR_INVALID;
+  if (dev_slots->num_layers != host->num_layers || dev_slots->num_heads != host->num_heads ||
+      dev_slots->head_dim != host->head_dim || dev_slots->batch != host->batch ||
+      dev_slots->elem_bytes != host->elem_bytes)
+    return DV_ERR_INVALID;
+  uint64_t bytes = 0;
+  int rc = dv_cache_bytes(dev_slots, &bytes);
+  if (rc != DV_OK) return rc;
+  rc = dv_cache_bytes(host, &bytes);
+  if (rc != DV_OK) return rc;
+  dv_swapper* s = new (std::nothrow) dv_swapper();
+  if (!s) return DV_ERR_INVALID;
+  // Own copies of the base arrays: the caller's may go away after this call.
+  s->dev = *dev_slots;
+  s->host = *host;
+  s->dev_base.assign(dev_slots->mb_base, dev_slots->mb_base + 2);
+  s->host_base.assign(host->mb_base, host->mb_base + host->num_mb);
+  s->dev.num_mb = 2;
+  s->dev.mb_base = s->dev_base.data();
+  s->host.mb_base = s->host_base.data();
+  s->slot_of.assign(host->num_mb, -1);
+  // Streams at the default priority.
+  if (hipStreamCreateWithFlags(&s->s_in, hipStreamNonBlocking) != hipSuccess ||
+      hipStreamCreateWithFlags(&s->s_out, hipStreamNonBlocking) != hipSuccess) {
+    release(s);
+    return DV_ERR_HIP;
+  }
+  for (int i = 0; i < 2; ++i) {
+    if (hipEventCreateWithFlags(&s->resident[i], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&s->freed[i], hipEventDisableTiming) != hipSuccess) {
+      release(s);
+      return DV_ERR_HIP;
+    }
+  }
+  if (hipEventCreateWithFlags(&s->step_done, hipEventDisableTiming) != hipSuccess) {
+    release(s);
+    return DV_ERR_HIP;
+  }
+  *out = s;
+  return DV_OK;
+}
+
+int dv_swapper_destroy(dv_swapper* s) {
+  if (!s) return DV_ERR_INVALID;
+  release(s);
+  return DV_OK;
+}
+
+int dv_swapper_prefetch(dv_swapper* s, int32_t mb, const int32_t* len) {
+  if (!s || !len) return DV_ERR_INVALID;
+  if (mb < 0 || mb >= s->host.num_mb) return DV_ERR_RANGE;
+  if (s->slot_of[mb] >= 0) return DV_OK;  // already resident or on its way
+  const int slot = s->next_slot;
+  const int prev = s->occupant[slot];
+  if (!s->done[slot]) return DV_ERR_INVALID;  // occupant's step has not ended
+  if (prev >= 0) s->slot_of[prev] = -1;
+  // The slot is reused only after its previous occupant's update has left.
+  if (prev >= 0 && hipStreamWaitEvent(s->s_in, s->freed[slot], 0) != hipSuccess)
+    return DV_ERR_HIP;
+  int rc = dv_swap_in(&s->host, mb, &s->dev, slot, 0, s->host.num_layers, nullptr, len, s->s_in);
+  if (rc != DV_OK) return rc;
+  rc = hip_ok(hipEventRecord(s->resident[slot], s->s_in));
+  if (rc != DV_OK) return rc;
+  s->occupant[slot] = mb;
+  s->slot_of[mb] = slot;
+  s->done[slot] = false;
+  s->next_slot ^= 1;
+  return DV_OK;
+}
+
+int dv_swapper_begin_step(dv_swapper* s, int32_t mb, void* compute_stream, int32_t* slot_out) {
+  if (!s || !slot_out) return DV_ERR_INVALID;
+  if (mb < 0 || mb >= s->host.num_mb) return DV_ERR_RANGE;
+  const int slot = s->slot_of[mb];
+  if (slot < 0) return DV_ERR_RANGE;  // not prefetched
+  if (hipStreamWaitEvent(static_cast<hipStream_t>(compute_stream), s->resident[slot], 0) !=
+      hipSuccess)
+    return DV_ERR_HIP;
+  *slot_out = slot;
+  return DV_OK;
+}
+
+int dv_swapper_end_step(dv_swapper* s, int32_t mb, void* compute_stream, const int32_t* t0,
+                        const int32_t* t1) {
+  if (!s || !t1) return DV_ERR_INVALID;
+  if (mb < 0 || mb >= s->host.num_mb) return DV_ERR_RANGE;
+  const int slot = s->slot_of[mb];
+  if (slot < 0) return DV_ERR_RANGE;
+  int rc = hip_ok(hipEventRecord(s->step_done, static_cast<hipStream_t>(compute_stream)));
+  if (rc != DV_OK) return rc;
+  if (hipStreamWaitEvent(s->s_out, s->step_done, 0) != hipSuccess) return DV_ERR_HIP;
+  rc = dv_swap_out(&s->dev, slot, &s->host, mb, 0, s->host.num_layers, t0, t1, s->s_out);
+  if (rc != DV_OK) return rc;
+  rc = hip_ok(hipEventRecord(s->freed[slot], s->s_out));
+  if (rc == DV_OK) s->done[slot] = true;
+  return rc;
+}
+
+int dv_swapper_sync(dv_swapper* s) {
+  if (!s) return DV_ERR_INVALID;
+  if (hipStreamSynchronize(s->s_in) != hipSuccess) return DV_ERR_HIP;
+  if (hipStreamSynchronize(s->s_out) != hipSuccess) return DV_ERR_HIP;
+  return DV_OK;
+}
+
+}  // extern "C"

@@ -70,6 +70,12 @@ def _load():
         "dv_swap_out": [P, i32, P, i32, i32, i32, vp, vp, vp],
         "dv_swap_in": [P, i32, P, i32, i32, i32, vp, vp, vp],
         "dv_api_version": [],
+        "dv_swapper_create": [P, P, ctypes.POINTER(vp)],
+        "dv_swapper_prefetch": [vp, i32, vp],
+        "dv_swapper_begin_step": [vp, i32, vp, ctypes.POINTER(i32)],
+        "dv_swapper_end_step": [vp, i32, vp, vp, vp],
+        "dv_swapper_sync": [vp],
+        "dv_swapper_destroy": [vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -84,7 +90,9 @@ lib = _load()
 
 # Symbols include/dv.h declares (checked by the tests against the library).
 EXPORTS = ("dv_cache_bytes", "dv_packed_bytes", "dv_stream_out_prompt", "dv_stream_out_token",
-           "dv_stream_in", "dv_swap_out", "dv_swap_in", "dv_status_string", "dv_api_version")
+           "dv_stream_in", "dv_swap_out", "dv_swap_in", "dv_status_string", "dv_api_version",
+           "dv_swapper_create", "dv_swapper_prefetch", "dv_swapper_begin_step",
+           "dv_swapper_end_step", "dv_swapper_sync", "dv_swapper_destroy")
 
 
 def status_string(status: int) -> str:
@@ -209,3 +217,48 @@ def dv_swap_in(host: Cache, host_mb: int, dev: Cache, slot: int, l0: int, l1: in
 
 def dv_api_version() -> int:
     return lib.dv_api_version()
+
+
+class Swapper:
+    """The microbatch swap scheduler (dv_swapper_*); keeps its descriptors."""
+
+    def __init__(self, dev_slots: Cache, host: Cache):
+        self.dev, self.host = dev_slots, host
+        h = ctypes.c_void_p(0)
+        _check(lib.dv_swapper_create(dev_slots.ref, host.ref, ctypes.byref(h)),
+               "dv_swapper_create", True)
+        self.h = h
+
+    def prefetch(self, mb: int, lens, check: bool = True) -> int:
+        a, p = _i32(lens)
+        return _check(lib.dv_swapper_prefetch(self.h, mb, p), "dv_swapper_prefetch", check)
+
+    def begin_step(self, mb: int, stream=None) -> int:
+        slot = ctypes.c_int32(-1)
+        _check(lib.dv_swapper_begin_step(self.h, mb, _stream(stream), ctypes.byref(slot)),
+               "dv_swapper_begin_step", True)
+        return slot.value
+
+    def end_step(self, mb: int, t0, t1, stream=None, check: bool = True) -> int:
+        a0, p0 = _i32(t0)
+        a1, p1 = _i32(t1)
+        return _check(lib.dv_swapper_end_step(self.h, mb, _stream(stream), p0, p1),
+                      "dv_swapper_end_step", check)
+
+    def sync(self) -> None:
+        _check(lib.dv_swapper_sync(self.h), "dv_swapper_sync", True)
+
+    def close(self) -> None:
+        if self.h:
+            _check(lib.dv_swapper_destroy(self.h), "dv_swapper_destroy", True)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def dv_swapper_create(dev_slots: Cache, host: Cache) -> Swapper:
+    return Swapper(dev_slots, host)

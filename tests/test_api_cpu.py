@@ -161,3 +161,23 @@ def test_swap_rejections():
     assert dv.dv_swap_out(p, 0, h, 0, 0, 2, z, t1, check=False) == dv.DV_ERR_UNSUPPORTED
     # empty ranges are a no-op
     assert dv.dv_swap_out(d, 0, h, 0, 0, 2, z, z) == dv.DV_OK
+
+
+def test_swapper_create_rejections():
+    """Bad scheduler arguments are rejected before any stream is created."""
+    import ctypes as C
+    dev = dense(bases=(FAKE, FAKE + (1 << 32)))
+    host = dense(bases=(FAKE + (1 << 34),) * 4, mem=dv.DV_MEM_HOST_PINNED, S=64)
+    h = C.c_void_p(0)
+    one_slot = dense(bases=(FAKE,))
+    assert dv.lib.dv_swapper_create(one_slot.ref, host.ref, C.byref(h)) == dv.DV_ERR_INVALID
+    assert dv.lib.dv_swapper_create(host.ref, dev.ref, C.byref(h)) == dv.DV_ERR_INVALID
+    other = dense(H=4, bases=(FAKE + (1 << 34),) * 4, mem=dv.DV_MEM_HOST_PINNED)
+    assert dv.lib.dv_swapper_create(dev.ref, other.ref, C.byref(h)) == dv.DV_ERR_INVALID
+    paged = dv.Cache(dv.DV_PAGED, 2, 3, 64, 4, [FAKE, FAKE], block_size=16, num_blocks=8,
+                     max_blocks=4, block_tables=[FAKE, FAKE])
+    assert dv.lib.dv_swapper_create(paged.ref, host.ref, C.byref(h)) == dv.DV_ERR_UNSUPPORTED
+    assert dv.lib.dv_swapper_create(dev.ref, host.ref, None) == dv.DV_ERR_INVALID
+    assert h.value is None
+    for f in ("dv_swapper_sync", "dv_swapper_destroy"):
+        assert getattr(dv.lib, f)(None) == dv.DV_ERR_INVALID

@@ -200,3 +200,78 @@ def test_opt66b_round_robin_swapping(oracle_lib):
         dv.dv_swap_in(hh, x, ds, 0, 0, L, zero, lens[x], compute)
         compute.synchronize()
         G.assert_dense_ranges_equal(slots[0], refs[x], L, B, H, S, D, E, 0, L, zero, lens[x])
+
+
+def test_swapper_round_robin(oracle_lib):
+    """The scheduler runs the protocol of the previous test by itself: five
+    microbatches (an odd count, so slots alternate differently each round)
+    through two slots, three rounds, ragged per-sequence positions."""
+    L, H, D, B, E = 3, 4, 128, 3, 2
+    S, S_host, M = 64, 48, 5
+    dl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S, elem_bytes=E)
+    hl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S_host, elem_bytes=E)
+    slots = [G.dev_const(dl.storage_bytes(), 0) for _ in range(2)]
+    refs = [G.dev_filled(dl.storage_bytes(), 70 + x) for x in range(M)]
+    hosts = [pinned(hl.storage_bytes(), 0) for _ in range(M)]
+    ds = dv.Cache(dv.DV_DENSE, L, H, D, B, slots, max_seq=S)
+    dr = dv.Cache(dv.DV_DENSE, L, H, D, B, refs, max_seq=S)
+    hh = dv.Cache(dv.DV_DENSE, L, H, D, B, [t.data_ptr() for t in hosts], max_seq=S_host,
+                  mem=dv.DV_MEM_HOST_PINNED)
+    zero = np.zeros(B, np.int32)
+    lens = [np.array([20, 25, 30], np.int32) + x for x in range(M)]
+    compute = torch.cuda.current_stream()
+    for x in range(M):
+        dv.dv_swap_out(dr, x, hh, x, 0, L, zero, lens[x], compute)
+    compute.synchronize()
+    sw = dv.Swapper(ds, hh)
+    n = dv.dv_packed_bytes(ds, 0, L, lens[0], lens[0] + 1)
+    tok = torch.empty(n, dtype=torch.uint8, device=G.DEV)
+    inc = torch.empty(n, dtype=torch.uint8, device=G.DEV)
+    steps = 3 * M
+    sw.prefetch(0, lens[0])
+    for k in range(steps):
+        x = k % M
+        if k + 1 < steps:
+            xn = (k + 1) % M
+            sw.prefetch(xn, lens[xn])
+        slot = sw.begin_step(x, compute)
+        pos = lens[x]
+        synth.device_fill(tok.data_ptr(), n, 900 + k, stream=compute.cuda_stream)
+        dv.dv_stream_in(ds, slot, 0, L, pos, pos + 1, tok, n, compute)
+        dv.dv_stream_in(dr, x, 0, L, pos, pos + 1, tok, n, compute)
+        dv.dv_stream_out_token(ds, slot, 0, L, pos, inc, n, compute)
+        sw.end_step(x, pos, pos + 1, compute)
+        lens[x] = pos + 1
+        compute.synchronize()
+        assert torch.equal(inc, tok), k
+    sw.sync()
+    # every host mirror equals its reference on [0, len) (oracle copy map)
+    for x in range(M):
+        exp = np.zeros(hl.storage_bytes(), np.uint8)
+        oracle_lib.copy_ranges(dl, G.host(refs[x]), hl, exp, 0, L, zero, lens[x])
+        m = np.zeros(hl.storage_bytes(), np.uint8)
+        oracle_lib.copy_ranges(hl, hosts[x].numpy(), hl, m, 0, L, zero, lens[x])
+        assert m.tobytes() == exp.tobytes(), x
+    sw.close()
+
+
+def test_swapper_refuses_refill_before_step_end():
+    L, H, D, B = 1, 1, 64, 1
+    slots = [G.dev_const(L * 2 * B * H * 16 * D * 2, 0) for _ in range(2)]
+    hosts = [pinned(L * 2 * B * H * 16 * D * 2, 0) for _ in range(3)]
+    ds = dv.Cache(dv.DV_DENSE, L, H, D, B, slots, max_seq=16)
+    hh = dv.Cache(dv.DV_DENSE, L, H, D, B, [t.data_ptr() for t in hosts], max_seq=16,
+                  mem=dv.DV_MEM_HOST_PINNED)
+    sw = dv.Swapper(ds, hh)
+    lens = np.array([4], np.int32)
+    assert sw.prefetch(0, lens) == dv.DV_OK
+    assert sw.prefetch(1, lens) == dv.DV_OK
+    # both slots hold microbatches whose steps have not ended
+    assert sw.prefetch(2, lens, check=False) == dv.DV_ERR_INVALID
+    with pytest.raises(dv.DvError):
+        sw.begin_step(2)  # not prefetched
+    assert sw.begin_step(0) == 0
+    sw.end_step(0, [3], [4])
+    assert sw.prefetch(2, lens) == dv.DV_OK  # slot 0 is free again
+    sw.sync()
+    sw.close()
