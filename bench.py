@@ -43,7 +43,8 @@ if ROOT not in sys.path:
 # two), and with 4 queues the scheduler's input stream can land on the
 # compute stream's queue, which serialises every swap-in with the step it
 # should hide behind.  8 queues keep them apart.  Set before HIP starts.
-os.environ.setdefault("GPU_MAX_HW_QUEUES", "8")
+if int(os.environ.get("GPU_MAX_HW_QUEUES", "4") or 4) < 8:
+    os.environ["GPU_MAX_HW_QUEUES"] = "8"
 
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 PCIE_PEAK_GBS = 63.0        # PCIe Gen5 x16 per direction after 128b/130b encoding
@@ -478,6 +479,70 @@ def swap_protocol_bench(torch, dv, synth, swap_in_gbs):
     return res
 
 
+def buffered_vs_per_region(torch, dv, synth):
+    """The paper's buffered copies (pack into one temporary GPU buffer, then
+    one copy) against one copy call per contiguous region (Sec. 5.1, where
+    buffered copies were 95x faster streaming to remote CPU memory).  Here
+    on the OPT-13B stage, to pinned host memory and within HBM."""
+    from paper_2403_01876_amd import baseline
+    dev = torch.device("cuda:0")
+    w = synth.make_workload(1)
+    L, H, D, B, S = w.layers, w.heads, w.head_dim, w.batch, w.max_seq
+    st = torch.cuda.current_stream()
+    cache = torch.empty(w.dense_bytes(), dtype=torch.uint8, device=dev)
+    synth.device_fill(cache.data_ptr(), w.dense_bytes(), w.data_seed, stream=st.cuda_stream)
+    c = dv.Cache(dv.DV_DENSE, L, H, D, B, [cache], max_seq=S)
+    out = {}
+    cases = {"increment": (w.step_positions(0), w.step_positions(0) + 1),
+             "prompt": w.prompt_ranges()}
+    for name, (t0, t1) in cases.items():
+        n = dv.dv_packed_bytes(c, 0, L, t0, t1)
+        stage = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst_d = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst_h = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+        reps = 20 if name == "increment" else 3
+
+        def run(fn):
+            fn()
+            torch.cuda.synchronize()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            t_host = time.perf_counter()
+            a.record(st)
+            for _ in range(reps):
+                fn()
+            b.record(st)
+            torch.cuda.synchronize()
+            return min(a.elapsed_time(b), (time.perf_counter() - t_host) * 1e3) / reps, \
+                (time.perf_counter() - t_host) * 1e3 / reps
+
+        res = {"bytes": n}
+        for where, dst in (("to_host", dst_h), ("in_hbm", dst_d)):
+            def per_region():
+                baseline.per_region_copy(c, 0, 0, L, t0, t1, dst.data_ptr(), n, st)
+
+            def buffered():
+                if name == "increment":
+                    dv.dv_stream_out_token(c, 0, 0, L, t0, stage if where == "to_host" else dst,
+                                           n, st)
+                else:
+                    dv.dv_stream_out_prompt(c, 0, 0, L, t0, t1,
+                                            stage if where == "to_host" else dst, n, st)
+                if where == "to_host":
+                    dst.copy_(stage, non_blocking=True)
+
+            _, pr = run(per_region)
+            _, bf = run(buffered)
+            res[where] = {"per_region_ms": round(pr, 4), "buffered_ms": round(bf, 4),
+                          "speedup": round(pr / bf, 1),
+                          "regions": 2 * L * H * int((np.asarray(t1) > np.asarray(t0)).sum())}
+        out[name] = res
+        del stage, dst_d, dst_h
+    del cache
+    torch.cuda.empty_cache()
+    return out
+
+
 def read_link():
     """PCIe link speed/width of the GPU from sysfs (best effort)."""
     import glob
@@ -671,6 +736,8 @@ def main():
         log("extras: swap protocol")
         out["swap_protocol"] = swap_protocol_bench(torch, dv, synth,
                                                    out["swap"]["swap_in"]["GBps"])
+        log("extras: buffered vs per-region copies")
+        out["buffered_vs_per_region"] = buffered_vs_per_region(torch, dv, synth)
         log("extras: copy calibration")
         out["calibration_d2d_copy"] = copy_calibration(torch)
     if not args.no_cpu_baseline:

@@ -1,0 +1,42 @@
+"""ctypes binding of the per-region copy baseline (``libdv_baseline.so``).
+
+One copy call per contiguous region (the comparison baseline of the paper's
+evaluation, Sec. 5.1); used by the benchmark and its parity test only.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import dv
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdv_baseline.so")
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, i32 = ctypes.c_void_p, ctypes.c_int32
+        lib.dvb_per_region_copy.argtypes = [ctypes.POINTER(dv.dv_cache), i32, i32, i32, vp, vp,
+                                            vp, ctypes.c_uint64, vp]
+        lib.dvb_per_region_copy.restype = ctypes.c_int64
+        _lib = lib
+    return _lib
+
+
+def per_region_copy(cache: dv.Cache, mb: int, l0: int, l1: int, t0, t1, dst, dst_cap: int,
+                    stream=None) -> int:
+    """Returns the number of copy calls issued."""
+    a0 = np.ascontiguousarray(t0, dtype=np.int32)
+    a1 = np.ascontiguousarray(t1, dtype=np.int32)
+    n = _load().dvb_per_region_copy(cache.ref, mb, l0, l1, a0.ctypes.data, a1.ctypes.data,
+                                    dv._addr(dst), dst_cap, dv._stream(stream))
+    if n < 0:
+        raise dv.DvError(int(n), "dvb_per_region_copy")
+    return int(n)

@@ -10,6 +10,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIBDV = os.path.join(PKG, "libdv.so")
 LIBSYNTH = os.path.join(ROOT, "synth", "libdvsynth.so")
+LIBBASE = os.path.join(PKG, "libdv_baseline.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # -packed-fp32-ops: keep the compiler from emitting packed fp32 instructions
@@ -32,6 +33,16 @@ def build_libdv(out: str = LIBDV) -> str:
     return out
 
 
+def build_baseline(out: str = LIBBASE) -> str:
+    """The per-region copy baseline the benchmark compares against."""
+    src = os.path.join(PKG, "csrc", "dv_baseline.cpp")
+    tmp = out + ".tmp"
+    _run([HIPCC, *HIP_FLAGS, "-x", "hip", src, "-L" + PKG, "-ldv",
+          "-Wl,-rpath,$ORIGIN", "-o", tmp])
+    os.replace(tmp, out)
+    return out
+
+
 def build_libsynth(out: str = LIBSYNTH) -> str:
     src = os.path.join(ROOT, "synth", "csrc", "gen_fill.hip")
     tmp = out + ".tmp"
@@ -42,6 +53,7 @@ def build_libsynth(out: str = LIBSYNTH) -> str:
 
 def build_all() -> None:
     build_libdv()
+    build_baseline()
     build_libsynth()
 
 

@@ -223,3 +223,30 @@ def test_graph_replay_matches_eager(oracle_lib):
         assert G.host(recv).tobytes() == exp.tobytes(), rep
         assert torch.equal(wire, eager_wire) and torch.equal(inc, eager_inc), rep
     del eager_recv
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_per_region_baseline_matches_buffered(oracle_lib, seed):
+    """The comparison baseline (one copy per contiguous region) yields the same
+    bytes as the buffered path, to device memory and to pinned host memory."""
+    from paper_2403_01876_amd import baseline
+    r = np.random.default_rng(40 + seed)
+    L, H, D, B, S = 2, int(r.integers(1, 5)), 128, int(r.integers(1, 7)), 90
+    lay = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S)
+    host = synth.fill_bytes(lay.storage_bytes(), seed)
+    cache = G.to_dev(host)
+    c = dv.Cache(dv.DV_DENSE, L, H, D, B, [cache], max_seq=S)
+    t0 = r.integers(0, 40, size=B).astype(np.int32)
+    t1 = (t0 + r.integers(0, 50, size=B)).astype(np.int32)
+    if seed == 3:
+        t1 = (t0 + 1).astype(np.int32)  # single tokens
+    exp = oracle_lib.pack(lay, host, 0, L, t0, t1)
+    n = exp.nbytes
+    d_buf = G.dev_const(max(n, 16), 0)
+    h_buf = torch.zeros(max(n, 16), dtype=torch.uint8, pin_memory=True)
+    calls = baseline.per_region_copy(c, 0, 0, L, t0, t1, d_buf, n, stream())
+    assert calls == 2 * L * H * int((t1 > t0).sum())
+    baseline.per_region_copy(c, 0, 0, L, t0, t1, h_buf.data_ptr(), n, stream())
+    torch.cuda.synchronize()
+    assert G.host(d_buf)[:n].tobytes() == exp.tobytes()
+    assert h_buf.numpy()[:n].tobytes() == exp.tobytes()
