@@ -46,6 +46,9 @@ extern "C" {
 
 #define DV_API_VERSION 1
 
+/* The library is built with hidden visibility; only these calls export. */
+#define DV_API __attribute__((visibility("default")))
+
 typedef enum {
   DV_OK = 0,
   DV_ERR_INVALID = -1,     /* malformed descriptor or argument: null pointer, extent <= 0,
@@ -115,11 +118,11 @@ typedef struct dv_cache {
 
 /* Storage bytes of one microbatch of `c` (dense: L*2*B*H*S*D*E; paged:
  * L*2*NB*H*bs*D*E).  Host-only.  DV_OK, DV_ERR_INVALID. */
-int dv_cache_bytes(const dv_cache* c, uint64_t* out_bytes);
+DV_API int dv_cache_bytes(const dv_cache* c, uint64_t* out_bytes);
 
 /* Bytes of the contiguous buffer for these ranges (formula above).  t0 may
  * be NULL (all zero).  Host-only.  DV_OK, DV_ERR_INVALID, DV_ERR_RANGE. */
-int dv_packed_bytes(const dv_cache* c, int32_t l0, int32_t l1, const int32_t* t0,
+DV_API int dv_packed_bytes(const dv_cache* c, int32_t l0, int32_t l1, const int32_t* t0,
                     const int32_t* t1, uint64_t* out_bytes);
 
 /* Pack microbatch `mb` of `src`, layers [l0, l1), tokens [t0[b], t1[b]) of
@@ -133,7 +136,7 @@ int dv_packed_bytes(const dv_cache* c, int32_t l0, int32_t l1, const int32_t* t0
  * [0, num_blocks) are rejected by no host check (the table is on the
  * device); the kernel skips them and their wire bytes are left unwritten.
  * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_HIP. */
-int dv_stream_out_prompt(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
+DV_API int dv_stream_out_prompt(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
                          const int32_t* t0, const int32_t* t1, void* dst, uint64_t dst_cap,
                          uint64_t* out_bytes, void* stream);
 
@@ -142,7 +145,7 @@ int dv_stream_out_prompt(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1
  * Identical to dv_stream_out_prompt with t0 = pos, t1 = pos + 1 (0 tokens
  * for inactive sequences), so the wire is [layer][K|V][active seq][head][D].
  * Same arguments, errors and ownership as dv_stream_out_prompt. */
-int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
+DV_API int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
                         const int32_t* pos, void* dst, uint64_t dst_cap, uint64_t* out_bytes,
                         void* stream);
 
@@ -155,7 +158,7 @@ int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
  * result is whichever write lands last; tokens with an unmapped entry are
  * skipped.  A token increment is streamed in with t0 = pos, t1 = pos + 1.
  * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_HIP. */
-int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
+DV_API int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
                  const int32_t* t1, const void* src, uint64_t src_bytes, void* stream);
 
 /* Microbatch swap-out: copy layers [l0, l1), tokens [t0[b], t1[b]) of device
@@ -172,12 +175,12 @@ int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const 
  * Swapping a whole microbatch passes its valid lengths; the step-t update
  * passes t0 = t, t1 = t + 1.
  * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_UNSUPPORTED, DV_ERR_HIP. */
-int dv_swap_out(const dv_cache* dev, int32_t slot, const dv_cache* host, int32_t host_mb,
+DV_API int dv_swap_out(const dv_cache* dev, int32_t slot, const dv_cache* host, int32_t host_mb,
                 int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1, void* stream);
 
 /* Microbatch swap-in (prefetch): the reverse copy, host microbatch
  * `host_mb` -> device slot `slot`.  Same rules as dv_swap_out. */
-int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev, int32_t slot,
+DV_API int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev, int32_t slot,
                int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1, void* stream);
 
 /* ------------------------------------------------------------------------
@@ -213,21 +216,52 @@ int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev, int32
  * begin/end of a microbatch not prefetched), DV_ERR_UNSUPPORTED, DV_ERR_HIP,
  * plus those of dv_swap_in / dv_swap_out. */
 typedef struct dv_swapper dv_swapper;
-int dv_swapper_create(const dv_cache* dev_slots, const dv_cache* host, dv_swapper** out);
-int dv_swapper_prefetch(dv_swapper* s, int32_t mb, const int32_t* len);
-int dv_swapper_begin_step(dv_swapper* s, int32_t mb, void* compute_stream, int32_t* slot_out);
-int dv_swapper_end_step(dv_swapper* s, int32_t mb, void* compute_stream, const int32_t* t0,
+DV_API int dv_swapper_create(const dv_cache* dev_slots, const dv_cache* host, dv_swapper** out);
+DV_API int dv_swapper_prefetch(dv_swapper* s, int32_t mb, const int32_t* len);
+DV_API int dv_swapper_begin_step(dv_swapper* s, int32_t mb, void* compute_stream, int32_t* slot_out);
+DV_API int dv_swapper_end_step(dv_swapper* s, int32_t mb, void* compute_stream, const int32_t* t0,
                         const int32_t* t1);
 /* Waits for all swaps queued so far. */
-int dv_swapper_sync(dv_swapper* s);
+DV_API int dv_swapper_sync(dv_swapper* s);
 /* Waits for queued swaps, then frees the scheduler's streams and events. */
-int dv_swapper_destroy(dv_swapper* s);
+DV_API int dv_swapper_destroy(dv_swapper* s);
+
+/* ------------------------------------------------------------------------
+ * Background streamer: layer-by-layer prompt streaming and token streaming
+ * in parallel with computation, driven by a background host thread
+ * (Sec. 4.1.1, optimisations 2 and 3).  The compute thread calls
+ * dv_streamer_push after queuing the work that produces a region on its
+ * compute stream; push records an event there and returns.  A worker thread
+ * then, on the streamer's own stream and after that event: packs the region
+ * (layers [l0, l1), tokens [t0[b], t1[b]) of microbatch `mb` of `src`, t0 may
+ * be NULL) into `staging` + staging_offset with dv_stream_out_prompt, and
+ * copies the packed bytes to `dst` + dst_offset (pinned host memory, or
+ * device memory).  Offsets are the caller's: pushing a prompt's layers one
+ * by one at offsets that accumulate their sizes leaves the whole prompt's
+ * contiguous buffer in `dst`, since layer ranges concatenate; decode steps
+ * can cycle through a few staging slots while filling a long host log.
+ * Pushes run in push order.  `staging` (device) and `dst` are caller owned,
+ * offsets 16-byte aligned, each must hold its offset + bytes (else
+ * DV_ERR_SPACE).  create allocates
+ * one stream, 64 events and the worker thread; push blocks only when 64
+ * pushes are waiting for the worker.  flush blocks until everything pushed
+ * has reached `dst` and returns the first error the worker met (a later
+ * push also returns it).  destroy drains, then frees.  Same alignment,
+ * range and layout rules as dv_stream_out_prompt. */
+typedef struct dv_streamer dv_streamer;
+DV_API int dv_streamer_create(const dv_cache* src, int32_t mb, void* staging, uint64_t staging_cap,
+                       void* dst, uint64_t dst_cap, dv_streamer** out);
+DV_API int dv_streamer_push(dv_streamer* s, void* compute_stream, int32_t l0, int32_t l1,
+                            const int32_t* t0, const int32_t* t1, uint64_t staging_offset,
+                            uint64_t dst_offset, uint64_t* out_bytes);
+DV_API int dv_streamer_flush(dv_streamer* s);
+DV_API int dv_streamer_destroy(dv_streamer* s);
 
 /* Static text for a dv_status value. */
-const char* dv_status_string(int status);
+DV_API const char* dv_status_string(int status);
 
 /* DV_API_VERSION of the built library. */
-int dv_api_version(void);
+DV_API int dv_api_version(void);
 
 #ifdef __cplusplus
 }

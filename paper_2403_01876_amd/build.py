@@ -15,7 +15,8 @@ LIBBASE = os.path.join(PKG, "libdv_baseline.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # -packed-fp32-ops: keep the compiler from emitting packed fp32 instructions
 # (none are needed; the kernels move bits only).
-HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-pthread",
+             "-fvisibility=hidden",
              "-Wall", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
@@ -26,7 +27,7 @@ def _run(cmd):
 
 def build_libdv(out: str = LIBDV) -> str:
     srcs = [os.path.join(PKG, "csrc", f) for f in ("dv_kernels.hip", "dv_api.cpp",
-                                                    "dv_swapper.cpp")]
+                                                    "dv_swapper.cpp", "dv_streamer.cpp")]
     tmp = out + ".tmp"
     _run([HIPCC, *HIP_FLAGS, "-x", "hip", *srcs, "-o", tmp])
     os.replace(tmp, out)

@@ -15,7 +15,7 @@ extern "C" {
 // one hipMemcpyAsync of the run of tokens [t0[b], t1[b]) into `dst` at its
 // position in the contiguous buffer order of include/dv.h.  Returns the
 // number of copy calls issued, or a negative dv_status.
-int64_t dvb_per_region_copy(const dv_cache* c, int32_t mb, int32_t l0, int32_t l1,
+DV_API int64_t dvb_per_region_copy(const dv_cache* c, int32_t mb, int32_t l0, int32_t l1,
                             const int32_t* t0, const int32_t* t1, void* dst, uint64_t dst_cap,
                             void* stream) {
   if (!c || c->kind != DV_DENSE || !c->mb_base || mb < 0 || mb >= c->num_mb || !t0 || !t1 ||

@@ -1,0 +1,222 @@
+// Background cache streamer: the paper's layer-by-layer prompt streaming and
+// token streaming in parallel with computation (Sec. 4.1.1, optimisations 2
+// and 3), driven by a background host thread as the paper describes.
+//
+// The compute thread calls dv_streamer_push after queuing the work that
+// produces a region (a prompt layer, a decode step's token).  push records
+// an event on the compute stream and hands a request to the worker thread;
+// the worker makes the streamer's side stream wait on that event, packs the
+// region into device staging (the buffered copy of optimisation 1) and copies
+// the staged chunk to its destination.  The compute thread pays one event
+// record and a queue push per region; the GPU overlaps the streaming with
+// whatever the compute stream runs next.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <condition_variable>
+#include <deque>
+#include <mutex>
+#include <new>
+#include <thread>
+#include <vector>
+
+#include "../../include/dv.h"
+
+namespace {
+
+constexpr int kEventPool = 64;
+
+struct Request {
+  int32_t l0, l1;
+  std::vector<int32_t> t0, t1;
+  uint64_t staging_off, dst_off, bytes;
+  int event;  // index into the pool
+};
+
+}  // namespace
+
+struct dv_streamer {
+  dv_cache src;
+  std::vector<void*> bases;
+  std::vector<const int32_t*> tables;
+  int32_t mb = 0;
+  char* staging = nullptr;
+  uint64_t staging_cap = 0;
+  char* dst = nullptr;
+  uint64_t dst_cap = 0;
+  int device = 0;
+  hipStream_t side = nullptr;
+  hipEvent_t events[kEventPool] = {};
+  std::vector<int> free_events;
+  std::deque<Request> queue;
+  int busy = 0;  // requests taken by the worker and not yet enqueued
+  int error = DV_OK;
+  bool stop = false;
+  std::mutex m;
+  std::condition_variable cv;
+  std::thread worker;
+};
+
+namespace {
+
+void run_worker(dv_streamer* s) {
+  (void)hipSetDevice(s->device);
+  for (;;) {
+    Request r;
+    {
+      std::unique_lock<std::mutex> lk(s->m);
+      s->cv.wait(lk, [s] { return s->stop || !s->queue.empty(); });
+      if (s->queue.empty()) return;  // stop requested and nothing left
+      r = std::move(s->queue.front());
+      s->queue.pop_front();
+      ++s->busy;
+    }
+    int rc = DV_OK;
+    // The wait captures the event's current record, so the event can be
+    // handed back for reuse as soon as the wait is queued.
+    if (hipStreamWaitEvent(s->side, s->events[r.event], 0) != hipSuccess) rc = DV_ERR_HIP;
+    {
+      std::lock_guard<std::mutex> lk(s->m);
+      s->free_events.push_back(r.event);
+    }
+    s->cv.notify_all();
+    if (rc == DV_OK && r.bytes > 0) {
+      rc = dv_stream_out_prompt(&s->src, s->mb, r.l0, r.l1, r.t0.data(), r.t1.data(),
+                                s->staging + r.staging_off, r.bytes, nullptr, s->side);
+      if (rc == DV_OK &&
+          hipMemcpyAsync(s->dst + r.dst_off, s->staging + r.staging_off, r.bytes,
+                         hipMemcpyDefault, s->side) != hipSuccess)
+        rc = DV_ERR_HIP;
+    }
+    {
+      std::lock_guard<std::mutex> lk(s->m);
+      if (rc != DV_OK && s->error == DV_OK) s->error = rc;
+      --s->busy;
+    }
+    s->cv.notify_all();
+  }
+}
+
+void release(dv_streamer* s) {
+  if (s->worker.joinable()) {
+    {
+      std::lock_guard<std::mutex> lk(s->m);
+      s->stop = true;
+    }
+    s->cv.notify_all();
+    s->worker.join();
+  }
+  if (s->side) (void)hipStreamSynchronize(s->side);
+  for (hipEvent_t e : s->events)
+    if (e) (void)hipEventDestroy(e);
+  if (s->side) (void)hipStreamDestroy(s->side);
+  delete s;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int dv_streamer_create(const dv_cache* src, int32_t mb, void* staging, uint64_t staging_cap,
+                       void* dst, uint64_t dst_cap, dv_streamer** out) {
+  if (!src || !out || !src->mb_base || !staging || !dst || !aligned16(staging) ||
+      !aligned16(dst))
+    return DV_ERR_INVALID;
+  uint64_t bytes = 0;
+  int rc = dv_cache_bytes(src, &bytes);
+  if (rc != DV_OK) return rc;
+  if (mb < 0 || mb >= src->num_mb) return DV_ERR_RANGE;
+  dv_streamer* s = new (std::nothrow) dv_streamer();
+  if (!s) return DV_ERR_INVALID;
+  s->src = *src;
+  s->bases.assign(src->mb_base, src->mb_base + src->num_mb);
+  s->src.mb_base = s->bases.data();
+  if (src->kind == DV_PAGED && src->block_table) {
+    s->tables.assign(src->block_table, src->block_table + src->num_mb);
+    s->src.block_table = s->tables.data();
+  }
+  s->mb = mb;
+  s->staging = static_cast<char*>(staging);
+  s->staging_cap = staging_cap;
+  s->dst = static_cast<char*>(dst);
+  s->dst_cap = dst_cap;
+  if (hipGetDevice(&s->device) != hipSuccess ||
+      hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking) != hipSuccess) {
+    release(s);
+    return DV_ERR_HIP;
+  }
+  for (int i = 0; i < kEventPool; ++i) {
+    if (hipEventCreateWithFlags(&s->events[i], hipEventDisableTiming) != hipSuccess) {
+      release(s);
+      return DV_ERR_HIP;
+    }
+    s->free_events.push_back(i);
+  }
+  s->worker = std::thread(run_worker, s);
+  *out = s;
+  return DV_OK;
+}
+
+int dv_streamer_push(dv_streamer* s, void* compute_stream, int32_t l0, int32_t l1,
+                     const int32_t* t0, const int32_t* t1, uint64_t staging_offset,
+                     uint64_t dst_offset, uint64_t* out_bytes) {
+  if (!s || !t1) return DV_ERR_INVALID;
+  uint64_t bytes = 0;
+  int rc = dv_packed_bytes(&s->src, l0, l1, t0, t1, &bytes);
+  if (rc != DV_OK) return rc;
+  if (out_bytes) *out_bytes = bytes;
+  if (staging_offset % 16 != 0 || dst_offset % 16 != 0) return DV_ERR_INVALID;
+  if (staging_offset > s->staging_cap || bytes > s->staging_cap - staging_offset ||
+      dst_offset > s->dst_cap || bytes > s->dst_cap - dst_offset)
+    return DV_ERR_SPACE;
+  Request r;
+  r.l0 = l0;
+  r.l1 = l1;
+  const int32_t B = s->src.batch;
+  r.t0.assign(B, 0);
+  if (t0) r.t0.assign(t0, t0 + B);
+  r.t1.assign(t1, t1 + B);
+  r.staging_off = staging_offset;
+  r.dst_off = dst_offset;
+  r.bytes = bytes;
+  {
+    std::unique_lock<std::mutex> lk(s->m);
+    if (s->error != DV_OK) return s->error;
+    s->cv.wait(lk, [s] { return !s->free_events.empty(); });
+    r.event = s->free_events.back();
+    s->free_events.pop_back();
+  }
+  if (hipEventRecord(s->events[r.event], static_cast<hipStream_t>(compute_stream)) !=
+      hipSuccess) {
+    std::lock_guard<std::mutex> lk(s->m);
+    s->free_events.push_back(r.event);
+    return DV_ERR_HIP;
+  }
+  {
+    std::lock_guard<std::mutex> lk(s->m);
+    s->queue.push_back(std::move(r));
+  }
+  s->cv.notify_all();
+  return DV_OK;
+}
+
+int dv_streamer_flush(dv_streamer* s) {
+  if (!s) return DV_ERR_INVALID;
+  {
+    std::unique_lock<std::mutex> lk(s->m);
+    s->cv.wait(lk, [s] { return s->queue.empty() && s->busy == 0; });
+  }
+  if (hipStreamSynchronize(s->side) != hipSuccess) return DV_ERR_HIP;
+  std::lock_guard<std::mutex> lk(s->m);
+  return s->error;
+}
+
+int dv_streamer_destroy(dv_streamer* s) {
+  if (!s) return DV_ERR_INVALID;
+  release(s);
+  return DV_OK;
+}
+
+}  // extern "C"

@@ -76,6 +76,10 @@ def _load():
         "dv_swapper_end_step": [vp, i32, vp, vp, vp],
         "dv_swapper_sync": [vp],
         "dv_swapper_destroy": [vp],
+        "dv_streamer_create": [P, i32, vp, u64, vp, u64, ctypes.POINTER(vp)],
+        "dv_streamer_push": [vp, vp, i32, i32, vp, vp, u64, u64, u64p],
+        "dv_streamer_flush": [vp],
+        "dv_streamer_destroy": [vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -92,7 +96,8 @@ lib = _load()
 EXPORTS = ("dv_cache_bytes", "dv_packed_bytes", "dv_stream_out_prompt", "dv_stream_out_token",
            "dv_stream_in", "dv_swap_out", "dv_swap_in", "dv_status_string", "dv_api_version",
            "dv_swapper_create", "dv_swapper_prefetch", "dv_swapper_begin_step",
-           "dv_swapper_end_step", "dv_swapper_sync", "dv_swapper_destroy")
+           "dv_swapper_end_step", "dv_swapper_sync", "dv_swapper_destroy",
+           "dv_streamer_create", "dv_streamer_push", "dv_streamer_flush", "dv_streamer_destroy")
 
 
 def status_string(status: int) -> str:
@@ -262,3 +267,42 @@ class Swapper:
 
 def dv_swapper_create(dev_slots: Cache, host: Cache) -> Swapper:
     return Swapper(dev_slots, host)
+
+
+class Streamer:
+    """The background streamer (dv_streamer_*); keeps its descriptor."""
+
+    def __init__(self, src: Cache, mb: int, staging, staging_cap: int, dst, dst_cap: int):
+        self.src = src
+        h = ctypes.c_void_p(0)
+        _check(lib.dv_streamer_create(src.ref, mb, _addr(staging), staging_cap, _addr(dst),
+                                      dst_cap, ctypes.byref(h)), "dv_streamer_create", True)
+        self.h = h
+
+    def push(self, l0: int, l1: int, t0, t1, staging_offset: int, dst_offset=None,
+             stream=None, check: bool = True):
+        """Returns the region's size in bytes (or (status, bytes) with check=False).
+        ``dst_offset`` defaults to ``staging_offset``."""
+        a0, p0 = _i32(t0)
+        a1, p1 = _i32(t1)
+        out = ctypes.c_uint64(0)
+        if dst_offset is None:
+            dst_offset = staging_offset
+        rc = lib.dv_streamer_push(self.h, _stream(stream), l0, l1, p0, p1, staging_offset,
+                                  dst_offset, ctypes.byref(out))
+        _check(rc, "dv_streamer_push", check)
+        return out.value if check else (rc, out.value)
+
+    def flush(self, check: bool = True) -> int:
+        return _check(lib.dv_streamer_flush(self.h), "dv_streamer_flush", check)
+
+    def close(self) -> None:
+        if self.h:
+            _check(lib.dv_streamer_destroy(self.h), "dv_streamer_destroy", True)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -30,8 +30,10 @@ __global__ void __launch_bounds__(256) fill_kernel(ulonglong2* __restrict__ out,
 
 }  // namespace
 
-extern "C" int dvsynth_fill(void* dev, uint64_t nbytes, uint64_t seed, uint64_t first_byte,
-                            void* stream) {
+extern "C" __attribute__((visibility("default"))) int dvsynth_fill(void* dev, uint64_t nbytes,
+                                                                 uint64_t seed,
+                                                                 uint64_t first_byte,
+                                                                 void* stream) {
   if (dev == nullptr || (nbytes % 16) != 0 || (first_byte % 16) != 0 ||
       (reinterpret_cast<uintptr_t>(dev) % 16) != 0)
     return -1;

@@ -181,3 +181,23 @@ def test_swapper_create_rejections():
     assert h.value is None
     for f in ("dv_swapper_sync", "dv_swapper_destroy"):
         assert getattr(dv.lib, f)(None) == dv.DV_ERR_INVALID
+
+
+def test_streamer_create_rejections():
+    import ctypes as C
+    c = dense()
+    h = C.c_void_p(0)
+    st = FAKE + (1 << 33)
+    assert dv.lib.dv_streamer_create(None, 0, st, 1 << 20, st, 1 << 20, C.byref(h)) == \
+        dv.DV_ERR_INVALID
+    assert dv.lib.dv_streamer_create(c.ref, 1, st, 1 << 20, st, 1 << 20, C.byref(h)) == \
+        dv.DV_ERR_RANGE
+    assert dv.lib.dv_streamer_create(c.ref, 0, st + 8, 1 << 20, st, 1 << 20, C.byref(h)) == \
+        dv.DV_ERR_INVALID
+    assert dv.lib.dv_streamer_create(c.ref, 0, None, 1 << 20, st, 1 << 20, C.byref(h)) == \
+        dv.DV_ERR_INVALID
+    assert dv.lib.dv_streamer_create(dense(D=36).ref, 0, st, 1 << 20, st, 1 << 20,
+                                     C.byref(h)) == dv.DV_ERR_INVALID
+    assert h.value is None
+    for f in ("dv_streamer_flush", "dv_streamer_destroy"):
+        assert getattr(dv.lib, f)(None) == dv.DV_ERR_INVALID

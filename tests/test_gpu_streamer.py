@@ -1,0 +1,105 @@
+"""The background streamer: layer-by-layer prompt streaming and token
+streaming overlapped with the compute stream (checked against the oracle)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2403_01876_amd import dv  # noqa: E402
+from tests import gpu_util as G  # noqa: E402
+
+
+def test_layer_by_layer_prompt_to_host(oracle_lib):
+    """Each layer is written by the compute stream just before it is pushed;
+    the host buffer ends up holding the whole prompt's contiguous buffer."""
+    L, H, D, B, S = 6, 3, 128, 4, 300
+    lay = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S)
+    cache = G.dev_const(lay.storage_bytes(), 0xA5)  # not yet computed
+    c = dv.Cache(dv.DV_DENSE, L, H, D, B, [cache], max_seq=S)
+    lens = np.array([300, 17, 0, 129], np.int32)
+    zero = np.zeros(B, np.int32)
+    total = dv.dv_packed_bytes(c, 0, L, zero, lens)
+    staging = G.dev_const(total, 0)
+    host = torch.full((total,), 0x11, dtype=torch.uint8, pin_memory=True)
+    layer_wires = [synth.fill_bytes(dv.dv_packed_bytes(c, l, l + 1, zero, lens), 10 + l)
+                   for l in range(L)]
+    dev_wires = [G.to_dev(wl) for wl in layer_wires]
+    torch.cuda.synchronize()
+    compute = torch.cuda.Stream()
+    s = dv.Streamer(c, 0, staging, total, host.data_ptr(), total)
+    off = 0
+    with torch.cuda.stream(compute):
+        for l in range(L):
+            # "compute" layer l: a long spin, then the layer's K/V land in the cache
+            torch.cuda._sleep(2_000_000)
+            dv.dv_stream_in(c, 0, l, l + 1, zero, lens, dev_wires[l], dev_wires[l].numel(),
+                            compute)
+            off += s.push(l, l + 1, zero, lens, off, stream=compute)
+    assert off == total
+    s.flush()
+    s.close()
+    torch.cuda.synchronize()
+    # expected: the cache after all layers, packed whole
+    exp_cache = np.full(lay.storage_bytes(), 0xA5, np.uint8)
+    for l in range(L):
+        oracle_lib.unpack(lay, exp_cache, l, l + 1, zero, lens, layer_wires[l])
+    exp = oracle_lib.pack(lay, exp_cache, 0, L, zero, lens)
+    assert host.numpy().tobytes() == exp.tobytes()
+
+
+def test_token_streaming_many_steps(oracle_lib):
+    """100 decode steps (more than the streamer's 64 events), each token
+    written by the compute stream and pushed to its own slot."""
+    L, H, D, B, S = 2, 2, 64, 3, 160
+    lay = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S)
+    host_cache = synth.fill_bytes(lay.storage_bytes(), 3)
+    cache = G.to_dev(host_cache)
+    c = dv.Cache(dv.DV_DENSE, L, H, D, B, [cache], max_seq=S)
+    steps = 100
+    base = np.array([10, 30, 50], np.int32)
+    inc = dv.dv_packed_bytes(c, 0, L, base, base + 1)
+    staging = G.dev_const(inc * 4, 0)  # 4 slots, reused
+    host = torch.zeros(inc * steps, dtype=torch.uint8, pin_memory=True)
+    tok_wires = [synth.fill_bytes(inc, 100 + i) for i in range(steps)]
+    dev_tok = [G.to_dev(t) for t in tok_wires]
+    torch.cuda.synchronize()
+    compute = torch.cuda.Stream()
+    s = dv.Streamer(c, 0, staging, inc * 4, host.data_ptr(), inc * steps)
+    with torch.cuda.stream(compute):
+        for i in range(steps):
+            p = base + i
+            dv.dv_stream_in(c, 0, 0, L, p, p + 1, dev_tok[i], inc, compute)
+            # staging slot i % 4, destination slot i
+            assert s.push(0, L, p, p + 1, (i % 4) * inc, i * inc, stream=compute) == inc
+    s.flush()
+    s.close()
+    torch.cuda.synchronize()
+    h = host.numpy()
+    for i in range(steps):
+        assert h[i * inc:(i + 1) * inc].tobytes() == tok_wires[i].tobytes(), i
+
+
+def test_streamer_errors_surface():
+    L, H, D, B, S = 1, 1, 64, 2, 16
+    cache = G.dev_const(L * 2 * B * H * S * D * 2, 0)
+    c = dv.Cache(dv.DV_DENSE, L, H, D, B, [cache], max_seq=S)
+    staging = G.dev_const(4096, 0)
+    dst = G.dev_const(4096, 0)
+    s = dv.Streamer(c, 0, staging, 4096, dst, 4096)
+    rc, n = s.push(0, 1, [0, 0], [17, 0], 0, check=False)
+    assert rc == dv.DV_ERR_RANGE
+    rc, n = s.push(0, 1, [0, 0], [16, 16], 0, check=False)
+    assert rc == dv.DV_ERR_SPACE and n == 2 * 2 * 16 * 64 * 2
+    rc, n = s.push(0, 1, [0, 0], [1, 1], 8, check=False)
+    assert rc == dv.DV_ERR_INVALID  # unaligned offset
+    rc, n = s.push(0, 1, [0, 0], [1, 1], 0, 4096, check=False)
+    assert rc == dv.DV_ERR_SPACE  # destination offset past the end
+    assert s.flush() == dv.DV_OK
+    s.close()
