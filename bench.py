@@ -543,6 +543,117 @@ def buffered_vs_per_region(torch, dv, synth):
     return out
 
 
+def overlap_bench(torch, dv, synth):
+    """Streaming overlapped with computation (the paper's optimisations 2
+    and 3 with a background thread), on the OPT-13B stage with emulated
+    compute of a 13B model's layer sizes (hidden 5120, 12 h^2 weights per
+    layer, bf16 GEMMs): a prompt pass over the stage's 10 layers, each
+    followed by streaming that layer's prompt cache to pinned host memory,
+    then 32 decode steps, each followed by streaming its increment.
+
+    Three runs: compute alone; compute with the background streamer
+    (overlapped); compute with the same packs and copies issued inline on
+    the compute stream (not overlapped)."""
+    dev = torch.device("cuda:0")
+    w = synth.make_workload(1)
+    L, H, D, B, S = w.layers, w.heads, w.head_dim, w.batch, w.max_seq
+    hidden = H * D
+    st = torch.cuda.current_stream()
+    cache = torch.empty(w.dense_bytes(), dtype=torch.uint8, device=dev)
+    synth.device_fill(cache.data_ptr(), w.dense_bytes(), w.data_seed, stream=st.cuda_stream)
+    c = dv.Cache(dv.DV_DENSE, L, H, D, B, [cache], max_seq=S)
+    t0, t1 = w.prompt_ranges()
+    P = dv.dv_packed_bytes(c, 0, L, t0, t1)
+    staging = torch.empty(P, dtype=torch.uint8, device=dev)
+    host = torch.empty(P, dtype=torch.uint8, pin_memory=True)
+    ntok = int(np.sum(t1))
+    g = torch.Generator(device=dev).manual_seed(0)
+    Wt = torch.randn(hidden, 12 * hidden, device=dev, dtype=torch.bfloat16, generator=g)
+    Xp = torch.randn(ntok, hidden, device=dev, dtype=torch.bfloat16, generator=g)
+    Xt = torch.randn(B, hidden, device=dev, dtype=torch.bfloat16, generator=g)
+    layer_off = []
+    off = 0
+    for l in range(L):
+        layer_off.append(off)
+        off += dv.dv_packed_bytes(c, l, l + 1, t0, t1)
+    steps = 32
+    pos = [w.step_positions(i) for i in range(steps)]
+    I = dv.dv_packed_bytes(c, 0, L, pos[0], pos[0] + 1)
+    ring = 4
+
+    def prompt_compute():
+        return torch.mm(Xp, Wt)
+
+    def token_compute():
+        for _ in range(L):
+            torch.mm(Xt, Wt)
+
+    for _ in range(2):  # warm the GEMMs
+        prompt_compute()
+        token_compute()
+    torch.cuda.synchronize()
+
+    def run(mode):
+        streamer = None
+        if mode == "overlapped":
+            streamer = dv.Streamer(c, 0, staging, P, host.data_ptr(), P)
+        a = torch.cuda.Event(enable_timing=True)
+        m = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(st)
+        for l in range(L):
+            prompt_compute()
+            n = dv.dv_packed_bytes(c, l, l + 1, t0, t1)
+            if mode == "overlapped":
+                streamer.push(l, l + 1, t0, t1, layer_off[l], stream=st)
+            elif mode == "inline":
+                dv.dv_stream_out_prompt(c, 0, l, l + 1, t0, t1,
+                                        staging[layer_off[l]:], n, st)
+                host[layer_off[l]:layer_off[l] + n].copy_(
+                    staging[layer_off[l]:layer_off[l] + n], non_blocking=True)
+        m.record(st)
+        for i in range(steps):
+            token_compute()
+            if mode == "overlapped":
+                streamer.push(0, L, pos[i], pos[i] + 1, (i % ring) * I, (i % ring) * I,
+                              stream=st)
+            elif mode == "inline":
+                so = (i % ring) * I
+                dv.dv_stream_out_token(c, 0, 0, L, pos[i], staging[so:], I, st)
+                host[so:so + I].copy_(staging[so:so + I], non_blocking=True)
+        b.record(st)
+        torch.cuda.synchronize()
+        if streamer is not None:
+            streamer.flush()
+        tail = torch.cuda.Event(enable_timing=True)
+        tail.record(st)
+        torch.cuda.synchronize()
+        res = {"prompt_ms": a.elapsed_time(m), "token_ms_per_step": m.elapsed_time(b) / steps}
+        if streamer is not None:
+            streamer.close()
+        return res
+
+    out = {"prompt_payload_bytes": P, "increment_bytes": I, "decode_steps": steps}
+    runs = {}
+    for mode in ("compute-only", "overlapped", "inline", "compute-only", "overlapped", "inline"):
+        r = run(mode)
+        if mode not in runs or r["prompt_ms"] < runs[mode]["prompt_ms"]:
+            runs[mode] = r
+    for mode, r in runs.items():
+        out[mode] = {k: round(v, 4) for k, v in r.items()}
+    base, ov, inl = runs["compute-only"], runs["overlapped"], runs["inline"]
+    out["prompt_slowdown_overlapped"] = round(ov["prompt_ms"] / base["prompt_ms"] - 1, 4)
+    out["prompt_slowdown_inline"] = round(inl["prompt_ms"] / base["prompt_ms"] - 1, 4)
+    out["token_slowdown_overlapped"] = round(ov["token_ms_per_step"] /
+                                             base["token_ms_per_step"] - 1, 4)
+    out["token_slowdown_inline"] = round(inl["token_ms_per_step"] /
+                                         base["token_ms_per_step"] - 1, 4)
+    del cache, staging, host, Wt, Xp, Xt
+    torch.cuda.empty_cache()
+    return out
+
+
 def read_link():
     """PCIe link speed/width of the GPU from sysfs (best effort)."""
     import glob
@@ -736,6 +847,8 @@ def main():
         log("extras: swap protocol")
         out["swap_protocol"] = swap_protocol_bench(torch, dv, synth,
                                                    out["swap"]["swap_in"]["GBps"])
+        log("extras: streaming overlapped with compute")
+        out["overlap"] = overlap_bench(torch, dv, synth)
         log("extras: buffered vs per-region copies")
         out["buffered_vs_per_region"] = buffered_vs_per_region(torch, dv, synth)
         log("extras: copy calibration")
