@@ -654,6 +654,60 @@ def overlap_bench(torch, dv, synth):
     return out
 
 
+def ring_recovery_bench(torch, dv, synth):
+    """Ring replication and the four-step recovery (Sec. 4.2.3) on one GPU:
+    four pipeline stages shaped like the BLOOM-176B shard (10 layers, 14 heads
+    x 128, batch 16) with two microbatches each, prompts of the shard
+    workload clipped to 1024 tokens, 16 decode steps with every step's
+    increment streamed to the next stage.  Stage 1 fails after computing
+    microbatch 1's step 12 and before streaming it; the recovery transfers
+    (replica back, predecessor's cache to the failed stage's replica slot)
+    are timed."""
+    from paper_2403_01876_amd.ring import RingSim
+    w = synth.make_workload(3)
+    lens = np.minimum(w.lens, 1024).astype(np.int32)
+    lens2 = np.minimum(w.lens[::-1], 1024).astype(np.int32)
+    sim = RingSim(workers=4, microbatches=2, layers=10, heads=14, head_dim=128, batch=16,
+                  max_seq=1024 + 16, prompt_lens=[lens, lens2], seed=3)
+    st = torch.cuda.current_stream()
+    sim.prefill()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(st)
+    stopped = sim.run((0, 0), (0, 16), fail_at=(1, 1, 12))
+    b.record(st)
+    torch.cuda.synchronize()
+    assert stopped
+    per_step = a.elapsed_time(b) / (12 * 2 + 2)
+    # bytes the recovery moves: stage 1's valid cache (from its replica) and
+    # stage 0's (into stage 1's replica slot)
+    zero = np.zeros(16, np.int32)
+    moved = 0
+    for j in range(2):
+        held = sim.table.steps_held(2, j)
+        moved += dv.dv_packed_bytes(sim.c[1], 0, 10, zero, sim.prompt[j] + held)
+        moved += dv.dv_packed_bytes(sim.c[0], 0, 10, zero,
+                                    sim.prompt[j] + sim._steps(sim.done[0], j))
+    sim.fail(1)
+    torch.cuda.synchronize()
+    a.record(st)
+    resume = sim.recover(1)
+    b.record(st)
+    torch.cuda.synchronize()
+    rec_ms = a.elapsed_time(b)
+    sim.run(resume, (0, 16))
+    torch.cuda.synchronize()
+    out = {"stages": 4, "microbatches": 2, "steps": 16, "failed_stage": 1,
+           "fail_after": [1, 12], "resume_point": list(resume),
+           "ms_per_step_all_stages_with_replication": round(per_step, 4),
+           "recovery_ms": round(rec_ms, 4), "recovery_bytes": moved,
+           "recovery_GBps_2x": round(2 * moved / (rec_ms * 1e-3) / 1e9, 1)}
+    del sim
+    torch.cuda.empty_cache()
+    return out
+
+
 def read_link():
     """PCIe link speed/width of the GPU from sysfs (best effort)."""
     import glob
@@ -849,6 +903,8 @@ def main():
                                                    out["swap"]["swap_in"]["GBps"])
         log("extras: streaming overlapped with compute")
         out["overlap"] = overlap_bench(torch, dv, synth)
+        log("extras: ring replication and recovery")
+        out["ring_recovery"] = ring_recovery_bench(torch, dv, synth)
         log("extras: buffered vs per-region copies")
         out["buffered_vs_per_region"] = buffered_vs_per_region(torch, dv, synth)
         log("extras: copy calibration")
