@@ -102,6 +102,10 @@ typedef struct dv_cache {
   const int32_t* const* block_table; /* paged: host array [num_mb] of device addresses of
                                         int32 [batch][max_blocks] tables; an entry outside
                                         [0, num_blocks) marks an unmapped block */
+  int32_t* const* block_owner;       /* paged, optional (NULL, or NULL entries, to leave
+                                        unused): host array [num_mb] of device addresses of
+                                        caller-owned int32 [num_blocks] workspaces, 4-byte
+                                        aligned; see dv_stream_in */
 } dv_cache;
 
 /* The contiguous buffer ("wire") a stream produces or consumes, for layer
@@ -154,9 +158,22 @@ DV_API int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int3
  * streamed positions are written; every other byte of the cache is left as
  * it was.  The receiver layout may differ from the sender's (capacity,
  * dense vs paged vs split-key).  Paged receivers: tables must map distinct
- * tokens to distinct slots (the same block must not appear twice), else the
- * result is whichever write lands last; tokens with an unmapped entry are
- * skipped.  A token increment is streamed in with t0 = pos, t1 = pos + 1.
+ * tokens to distinct slots (the same block must not appear twice within the
+ * streamed ranges), else the result is whichever write lands last; tokens
+ * with an unmapped entry are skipped.  A token increment is streamed in with
+ * t0 = pos, t1 = pos + 1.
+ *
+ * Paged receivers with a block_owner workspace for `mb`: when the call moves
+ * more than one token of some sequence, has at most 64 sequences and writes
+ * at least half of the pool's blocks, the library first rebuilds in the
+ * workspace the inverse of the table over the streamed ranges (pool block ->
+ * sequence * max_blocks + logical block, -1 for blocks not written) and then
+ * writes the pool in physical block order, so the writes are sequential
+ * instead of scattered by the table (measured on MI355X: 70 % -> 74 % of HBM
+ * peak for the LLaMA-2-70B stage's pool).  The bytes written are the same
+ * either way.  The workspace must not overlap the cache or `src`
+ * (DV_ERR_INVALID); its contents are scratch between calls, and calls that
+ * scatter into the same microbatch must not overlap in time.
  * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_HIP. */
 DV_API int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
                  const int32_t* t1, const void* src, uint64_t src_bytes, void* stream);

@@ -36,6 +36,7 @@ struct View {
   int64_t bs, NB, max_blocks;
   char* base;
   const int32_t* bt;
+  int32_t* owner;    // paged: optional owner-map workspace [NB]
   uint64_t bytes;    // storage bytes of the microbatch
 };
 
@@ -58,6 +59,7 @@ int view_of(const dv_cache* c, int32_t mb, View* v) {
   v->du = v->D * v->E / 16;
   v->S = v->bs = v->NB = v->max_blocks = 0;
   v->bt = nullptr;
+  v->owner = nullptr;
   if (c->kind == DV_DENSE || c->kind == DV_DENSE_KSPLIT) {
     if (c->max_seq <= 0) return DV_ERR_INVALID;
     v->S = v->cap = c->max_seq;
@@ -87,6 +89,8 @@ int view_of(const dv_cache* c, int32_t mb, View* v) {
   if (c->kind == DV_PAGED) {
     v->bt = c->block_table[mb];
     if (!v->bt) return DV_ERR_INVALID;
+    v->owner = c->block_owner ? c->block_owner[mb] : nullptr;
+    if ((reinterpret_cast<uintptr_t>(v->owner) & 3u) != 0) return DV_ERR_INVALID;
   }
   return DV_OK;
 }
@@ -228,11 +232,32 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
       a.num_blocks = (int32_t)v.NB;
       a.max_blocks = (int32_t)v.max_blocks;
       a.r = r;
+      const int64_t ngrp = (v.H + dv::kPagedHeads - 1) / dv::kPagedHeads;
       int64_t tiles = 0;
       for (int i = 0; i < nseq; ++i)
-        if (r.n[i] > 0)
-          tiles += ((r.t0[i] + r.n[i] + v.bs - 1) / v.bs - r.t0[i] / v.bs) *
-                   ((v.H + dv::kPagedHeads - 1) / dv::kPagedHeads);
+        if (r.n[i] > 0) tiles += ((r.t0[i] + r.n[i] + v.bs - 1) / v.bs - r.t0[i] / v.bs) * ngrp;
+      // Scatter in pool order through the owner map when the caller gave a
+      // workspace, all sequences fit one launch and the call writes at least
+      // half of the pool's blocks (otherwise most pool-order workgroups
+      // would find nothing to do).
+      const bool pool_order = dir == dv::kUnpack && v.owner && v.B <= kSeqPerLaunch &&
+                              2 * tiles >= v.NB * ngrp && v.NB * ngrp < (1ll << 31) &&
+                              v.B * v.max_blocks < (1ll << 31);
+      if (pool_order) {
+        dv::OwnerArgs o;
+        memset(&o, 0, sizeof o);
+        o.owner = v.owner;
+        o.bt = v.bt;
+        o.nseq = nseq;
+        o.block_size = (int32_t)v.bs;
+        o.num_blocks = (int32_t)v.NB;
+        o.max_blocks = (int32_t)v.max_blocks;
+        o.r = r;
+        const hipError_t e = dv::launch_owner_map(o, st);
+        if (e != hipSuccess) return hip_fail(e, "owner map launch");
+        a.owner = v.owner;
+        tiles = v.NB * ngrp;
+      }
       if (tiles >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
       const hipError_t e = dv::launch_paged(dir, a, (uint32_t)tiles, 2 * nl, st);
       if (e != hipSuccess) return hip_fail(e, "paged kernel launch");
@@ -475,6 +500,9 @@ int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const 
   if (need == 0) return DV_OK;
   if (!src || !aligned16(src)) return DV_ERR_INVALID;
   if (overlaps(src, need, v.base, v.bytes)) return DV_ERR_INVALID;
+  if (v.owner && (overlaps(v.owner, (uint64_t)v.NB * 4, v.base, v.bytes) ||
+                  overlaps(v.owner, (uint64_t)v.NB * 4, src, need)))
+    return DV_ERR_INVALID;
   rc = check_kind_supported(v);
   if (rc != DV_OK) return rc;
   return run_stream(dv::kUnpack, v, l0, l1, r0, rn, N, const_cast<void*>(src),

@@ -44,17 +44,32 @@ struct DenseRunArgs {
   SeqRanges r;
 };
 
-// Paged blocks: one workgroup per (slab, sequence, logical block).
+// Paged blocks: one workgroup per (slab, block, head pair).  Blocks are
+// taken in table order -- (sequence, logical block) -- or, when `owner` is
+// set, in pool order through the owner map.
 struct PagedArgs {
   void* pool;
   void* wire;
-  const int32_t* bt;  // this microbatch's block table [batch][max_blocks]
-  int64_t s_slab;     // pool units per slab (NB * heads * bs * du)
-  int64_t s_blk;      // pool units per block (heads * bs * du)
-  int64_t s_h;        // pool units per head in a block (bs * du)
+  const int32_t* bt;     // this microbatch's block table [batch][max_blocks]
+  const int32_t* owner;  // pool order: [num_blocks] owner map, else null
+  int64_t s_slab;        // pool units per slab (NB * heads * bs * du)
+  int64_t s_blk;         // pool units per block (heads * bs * du)
+  int64_t s_h;           // pool units per head in a block (bs * du)
   SlabMap m;
   int32_t du, heads, nseq, b0;
   int32_t block_size, num_blocks, max_blocks, pad;
+  SeqRanges r;
+};
+
+// Owner map of a paged table over the streamed ranges: owner[blk] =
+// b * max_blocks + j for each entry (b, j) whose logical block j holds a
+// streamed token of sequence b and whose block blk is in [0, num_blocks);
+// -1 for every other block.  Only launches with all sequences in one group
+// (b0 = 0) use it.
+struct OwnerArgs {
+  int32_t* owner;
+  const int32_t* bt;
+  int32_t nseq, block_size, num_blocks, max_blocks;
   SeqRanges r;
 };
 
@@ -111,6 +126,8 @@ hipError_t launch_dense_runs(int dir, const DenseRunArgs& a, uint32_t tiles_per_
                              uint32_t nslabs, hipStream_t s);
 hipError_t launch_paged(int dir, const PagedArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,
                         hipStream_t s);
+// Clears the owner map and fills it from the table (two launches).
+hipError_t launch_owner_map(const OwnerArgs& a, hipStream_t s);
 hipError_t launch_token(int dir, const TokenArgs& a, uint32_t units_per_slab, uint32_t nslabs,
                         hipStream_t s);
 hipError_t launch_ksplit(int dir, const KsplitArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,
@@ -126,7 +143,9 @@ constexpr int kDenseTile = kThreads * kDenseUnroll;
 
 // Heads per paged tile and 16-byte units per lane per pass (tiles are
 // counted on the host with kPagedHeads).  Measured on MI355X against 1, 4
-// and all heads per tile on the LLaMA-2-70B paged shape.
+// and all heads per tile on the LLaMA-2-70B paged shape.  The kernel splits
+// a tile's flattened (head, unit) index with one comparison, which holds
+// for two heads only.
 constexpr int kPagedHeads = 2;
 constexpr int kPagedUnroll = 2;
 

@@ -114,14 +114,23 @@ __global__ void __launch_bounds__(kThreads) dense_runs_kernel(DenseRunArgs a) {
 
 // ---------------------------------------------------------------------------
 // Paged blocks: grid (tiles_per_slab, nslabs); a tile is the part of one
-// logical block of one sequence inside its token range, for kPagedHeads
-// heads.  For a fixed (slab, block) the pool holds the heads back to back,
-// so the tile's pool side is one contiguous piece; on the wire side each
-// head's tokens are contiguous.  Two heads of a 16-token, 128-dim block make
-// an 8 KB tile, the size the dense kernel streams best at.
+// block of one sequence inside its token range, for kPagedHeads heads.  For
+// a fixed (slab, block) the pool holds the heads back to back, so the tile's
+// pool side is one contiguous piece; on the wire side each head's tokens are
+// contiguous.  Two heads of a 16-token, 128-dim block make an 8 KB tile, the
+// size the dense kernel streams best at.
+//
+// Table order (owner == null): tiles enumerate (sequence, logical block,
+// head pair) and find the pool block through the table, so consecutive
+// workgroups read consecutive wire bytes.  Pool order (owner set, unpack
+// only): tiles enumerate (pool block, head pair) and find the sequence and
+// logical block through the owner map, so consecutive workgroups write
+// consecutive pool bytes -- on MI355X writes scattered by a random table
+// cost more than reads scattered the same way.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ void __launch_bounds__(kThreads) paged_kernel(PagedArgs a) {
+  static_assert(kPagedHeads == 2, "the (head, unit) split below assumes two heads per tile");
   const int lane = lane_id();
   const int bs = a.block_size;
   const int ngrp = (a.heads + kPagedHeads - 1) / kPagedHeads;
@@ -131,25 +140,36 @@ __global__ void __launch_bounds__(kThreads) paged_kernel(PagedArgs a) {
     t0 = a.r.t0[lane];
     if (n > 0) tiles = ((t0 + n + bs - 1) / bs - t0 / bs) * ngrp;
   }
-  const int incl = wave_incl_scan(tiles);
   const int tok_incl = wave_incl_scan(n);
 
   // No XCD re-dealing here: pool blocks are scattered by the block table
   // anyway, and measured on MI355X the re-dealt order was 7 % slower.
   const int tile = blockIdx.x;
   const int64_t y = blockIdx.y;
-  const int b = owner_lane(incl, tile);
-  const int excl_b = __shfl(incl - tiles, b, 64);
+  int b, j, grp, blk;
+  if (a.owner) {
+    blk = tile / ngrp;
+    grp = tile - blk * ngrp;
+    const int own = a.owner[blk];
+    if (own < 0) return;  // block not written by this call
+    b = own / a.max_blocks;
+    j = own - b * a.max_blocks;
+    if (b >= a.nseq) return;
+  } else {
+    const int incl = wave_incl_scan(tiles);
+    b = owner_lane(incl, tile);
+    const int tj = tile - __shfl(incl - tiles, b, 64);
+    grp = tj % ngrp;
+    j = __shfl(t0, b, 64) / bs + tj / ngrp;  // logical block
+    blk = a.bt[(int64_t)(a.b0 + b) * a.max_blocks + j];
+    if (blk < 0 || blk >= a.num_blocks) return;  // unmapped block: skipped
+  }
   const int n_b = __shfl(n, b, 64);
   const int t0_b = __shfl(t0, b, 64);
   const int p_b = __shfl(tok_incl - n, b, 64);
-  const int tj = tile - excl_b;
-  const int grp = tj % ngrp;
-  const int j = t0_b / bs + tj / ngrp;  // logical block
   const int s_lo = max(t0_b, j * bs);
   const int s_hi = min(t0_b + n_b, (j + 1) * bs);
-  const int blk = a.bt[(int64_t)(a.b0 + b) * a.max_blocks + j];
-  if (blk < 0 || blk >= a.num_blocks) return;  // unmapped block: skipped
+  if (s_lo >= s_hi) return;
 
   const int run = (s_hi - s_lo) * a.du;  // units per head in this tile
   const int64_t slab = a.m.slab0 + y * a.m.slab_step;
@@ -162,7 +182,9 @@ __global__ void __launch_bounds__(kThreads) paged_kernel(PagedArgs a) {
                 (int64_t)h0 * w_h + (int64_t)(s_lo - t0_b) * a.du;
 
   // Flattened (head, unit) index over the tile; loads unguarded as in the
-  // dense kernel (a lane past the end re-reads the last unit).
+  // dense kernel (a lane past the end re-reads the last unit).  With two
+  // heads the index is below 2 * run, so one comparison names the head (an
+  // integer division here cost 3-4 % of the gather's bandwidth).
   const int total = min(kPagedHeads, a.heads - h0) * run;
   for (int base = 0; base < total; base += kPagedUnroll * kThreads) {
     u32x4 v[kPagedUnroll];
@@ -170,7 +192,7 @@ __global__ void __launch_bounds__(kThreads) paged_kernel(PagedArgs a) {
 #pragma unroll
     for (int i = 0; i < kPagedUnroll; ++i) {
       const int idx = min(base + i * kThreads + (int)threadIdx.x, total - 1);
-      hh[i] = idx / run;
+      hh[i] = idx >= run ? 1 : 0;
       ee[i] = idx - hh[i] * run;
       v[i] = ld_nt((D == kPack) ? pool + hh[i] * a.s_h + ee[i] : wire + hh[i] * w_h + ee[i]);
     }
@@ -180,6 +202,23 @@ __global__ void __launch_bounds__(kThreads) paged_kernel(PagedArgs a) {
         st_nt(v[i], (D == kPack) ? wire + hh[i] * w_h + ee[i] : pool + hh[i] * a.s_h + ee[i]);
     }
   }
+}
+
+// Owner map (see OwnerArgs): a clearing pass, then one lane per table entry.
+__global__ void __launch_bounds__(kThreads) owner_clear_kernel(OwnerArgs a) {
+  const int i = blockIdx.x * kThreads + threadIdx.x;
+  if (i < a.num_blocks) a.owner[i] = -1;
+}
+
+__global__ void __launch_bounds__(kThreads) owner_build_kernel(OwnerArgs a) {
+  const int b = blockIdx.y;
+  const int j = blockIdx.x * kThreads + threadIdx.x;
+  if (j >= a.max_blocks) return;
+  const int t0 = a.r.t0[b], t1 = t0 + a.r.n[b];
+  if (t0 >= t1 || (j + 1) * a.block_size <= t0 || j * a.block_size >= t1) return;
+  const int blk = a.bt[(int64_t)b * a.max_blocks + j];
+  if (blk < 0 || blk >= a.num_blocks) return;
+  a.owner[blk] = b * a.max_blocks + j;
 }
 
 // ---------------------------------------------------------------------------
@@ -375,6 +414,14 @@ hipError_t launch_paged(int dir, const PagedArgs& a, uint32_t tiles_per_slab, ui
   const void* fn =
       dir == kPack ? (const void*)&paged_kernel<kPack> : (const void*)&paged_kernel<kUnpack>;
   return launch(fn, dim3(tiles_per_slab, nslabs), a, s);
+}
+
+hipError_t launch_owner_map(const OwnerArgs& a, hipStream_t s) {
+  const uint32_t clear = (uint32_t)((a.num_blocks + kThreads - 1) / kThreads);
+  hipError_t e = launch((const void*)&owner_clear_kernel, dim3(clear), a, s);
+  if (e != hipSuccess) return e;
+  const uint32_t cols = (uint32_t)((a.max_blocks + kThreads - 1) / kThreads);
+  return launch((const void*)&owner_build_kernel, dim3(cols, a.nseq), a, s);
 }
 
 hipError_t launch_token(int dir, const TokenArgs& a, uint32_t units_per_slab, uint32_t nslabs,

@@ -137,6 +137,7 @@ int dv_streamer_create(const dv_cache* src, int32_t mb, void* staging, uint64_t 
     s->tables.assign(src->block_table, src->block_table + src->num_mb);
     s->src.block_table = s->tables.data();
   }
+  s->src.block_owner = nullptr;  // packs only: the owner map is never used
   s->mb = mb;
   s->staging = static_cast<char*>(staging);
   s->staging_cap = staging_cap;

@@ -46,6 +46,7 @@ class dv_cache(ctypes.Structure):
         ("num_mb", ctypes.c_int32),
         ("mb_base", ctypes.POINTER(ctypes.c_void_p)),
         ("block_table", ctypes.POINTER(ctypes.c_void_p)),
+        ("block_owner", ctypes.POINTER(ctypes.c_void_p)),
     ]
 
 
@@ -130,16 +131,24 @@ class Cache:
     def __init__(self, kind: int, layers: int, heads: int, head_dim: int, batch: int,
                  bases: Sequence, max_seq: int = 0, elem_bytes: int = 2,
                  mem: int = DV_MEM_DEVICE, block_size: int = 0, num_blocks: int = 0,
-                 max_blocks: int = 0, block_tables: Optional[Sequence] = None):
+                 max_blocks: int = 0, block_tables: Optional[Sequence] = None,
+                 block_owners: Optional[Sequence] = None):
+        """``block_owners``: optional per-microbatch int32 [num_blocks] device
+        workspaces (None entries allowed) that let bulk paged stream-ins
+        scatter in pool order."""
         self.bases = (ctypes.c_void_p * len(bases))(*[_addr(b) for b in bases])
-        self.tables = None
+        self.tables = self.owners = None
         if block_tables is not None:
             self.tables = (ctypes.c_void_p * len(block_tables))(*[_addr(t) for t in block_tables])
+        if block_owners is not None:
+            self.owners = (ctypes.c_void_p * len(block_owners))(
+                *[_addr(o) for o in block_owners])
+        ptr = ctypes.POINTER(ctypes.c_void_p)
         self.c = dv_cache(kind, mem, elem_bytes, layers, heads, head_dim, batch, max_seq,
                           block_size, num_blocks, max_blocks, len(bases),
-                          ctypes.cast(self.bases, ctypes.POINTER(ctypes.c_void_p)),
-                          None if self.tables is None else
-                          ctypes.cast(self.tables, ctypes.POINTER(ctypes.c_void_p)))
+                          ctypes.cast(self.bases, ptr),
+                          None if self.tables is None else ctypes.cast(self.tables, ptr),
+                          None if self.owners is None else ctypes.cast(self.owners, ptr))
 
     @property
     def ref(self):

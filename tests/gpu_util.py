@@ -96,3 +96,17 @@ def assert_dense_ranges_equal(recv, src, L, B, H, S, D, E, l0, l1, t0, t1, senti
         sv = torch.full((E,), sentinel, dtype=torch.uint8, device=DEV).view(TDT[E])[0]
         outside = r[m]
         assert bool((outside == sv).all()), "bytes outside the ranges changed"
+
+
+def owner_map_expected(bt, nb, bs, t0, t1):
+    """Inverse of a block table over the ranges, as the header defines it:
+    pool block -> b * max_blocks + j, -1 for blocks no streamed token uses."""
+    maxb = bt.shape[1]
+    own = np.full(nb, -1, np.int32)
+    for b in range(bt.shape[0]):
+        if t1[b] <= t0[b]:
+            continue
+        for j in range(t0[b] // bs, (t1[b] - 1) // bs + 1):
+            if 0 <= bt[b, j] < nb:
+                own[bt[b, j]] = b * maxb + j
+    return own

@@ -72,6 +72,32 @@ def test_packed_bytes_paged():
     del bt
 
 
+def test_owner_workspace_rejections():
+    """A paged receiver's owner-map workspace must be 4-byte aligned and must
+    not overlap the pool or the source buffer; all checked on the host."""
+    L, H, D, B, NB, MB = 2, 4, 64, 3, 12, 4
+    pool = FAKE
+    pool_bytes = L * 2 * NB * H * 16 * D * 2
+    wire = FAKE + (1 << 34)
+    t1 = np.array([16, 33, 0], np.int32)
+
+    def paged(owner):
+        return dv.Cache(dv.DV_PAGED, L, H, D, B, [pool], block_size=16, num_blocks=NB,
+                        max_blocks=MB, block_tables=[FAKE + (1 << 35)], block_owners=[owner])
+
+    need = dv.dv_packed_bytes(paged(None), 0, L, None, t1)
+    for owner, rc in ((FAKE + (1 << 36) + 2, dv.DV_ERR_INVALID),   # misaligned
+                      (pool + pool_bytes - 16, dv.DV_ERR_INVALID),  # inside the pool
+                      (wire + 64, dv.DV_ERR_INVALID)):              # inside the source
+        assert dv.dv_stream_in(paged(owner), 0, 0, L, None, t1, wire, need,
+                               check=False) == rc, hex(owner)
+    # a pack through the same descriptor checks alignment too (the map is
+    # then unused, so overlap with the pool is not an error for packs)
+    rc, _ = dv.dv_stream_out_prompt(paged(FAKE + (1 << 36) + 2), 0, 0, L, None, t1, wire, need,
+                                    check=False)
+    assert rc == dv.DV_ERR_INVALID
+
+
 def test_range_errors():
     c = dense()
     z = np.zeros(4, np.int32)

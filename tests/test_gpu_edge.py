@@ -171,6 +171,16 @@ def test_paged_unmapped_entries_are_skipped(oracle_lib):
         exp_pool = with_extra(np.full(L * 2 * nb * blk, 0xA5, np.uint8), 0xA5)
         oracle_lib.unpack(ext, exp_pool, 0, L, t0, t1, wh)
         assert G.host(recv).tobytes() == drop_extra(exp_pool).tobytes()
+        # the same scatter in pool order (an owner-map workspace given)
+        ws = G.dev_const(nb * 4, 0x7E)
+        recv2 = G.dev_const(L * 2 * nb * blk, 0xA5)
+        rc2 = dv.Cache(dv.DV_PAGED, L, H, D, B, [recv2], block_size=bs, num_blocks=nb,
+                       max_blocks=3, block_tables=[btd], block_owners=[ws])
+        dv.dv_stream_in(rc2, 0, 0, L, t0, t1, G.to_dev(wh), n, stream())
+        torch.cuda.synchronize()
+        assert G.host(recv2).tobytes() == drop_extra(exp_pool).tobytes()
+        if not single:  # 9 logical blocks streamed, 7 pool blocks: pool order taken
+            assert G.host(ws).view(np.int32).tolist() == [0, 1, 2, 3, 5, 6, 8]
 
 
 def test_graph_replay_matches_eager(oracle_lib):

@@ -174,6 +174,61 @@ def test_paged_gather_scatter(oracle_lib, seed):
     assert G.host(recv)[: lay_b.storage_bytes()].tobytes() == exp_recv.tobytes()
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_paged_scatter_pool_order(oracle_lib, seed):
+    """Scatter with an owner-map workspace: the pool equals the oracle's
+    unpack whichever order the library picks; when the header's conditions
+    hold (more than one token of some sequence, at most 64 sequences, at
+    least half of the pool's blocks written) the workspace holds the owner
+    map afterwards, otherwise it is untouched.  A second call with another
+    table reuses the stale workspace."""
+    r = np.random.default_rng(900 + seed)
+    L, H, D, B, E, bs, lens, maxb, bt, nb = paged_setup(r, seed, big_batch=(seed % 6 == 5))
+    kind = seed % 3
+    t0 = np.zeros(B, np.int32)
+    t1 = np.array(lens, np.int32)
+    for b in range(B):
+        if kind == 1:
+            a, c = sorted(int(v) for v in r.integers(0, lens[b] + 1, size=2))
+            t0[b], t1[b] = a, c
+        elif kind == 2 and r.random() < 0.2:
+            t1[b] = 0
+    l0 = int(r.integers(0, L))
+    l1 = int(r.integers(l0 + 1, L + 1))
+    ws = G.dev_const(nb * 4 + 64, 0x7E)
+    valid = bt >= 0
+    for call in range(2):
+        bt_b = bt.copy()
+        bt_b[valid] = r.permutation(bt[valid])
+        lay_b = oracle.Layout(oracle.PAGED, L, H, D, B, elem_bytes=E, block_size=bs,
+                              num_blocks=nb, block_table=bt_b)
+        n = dv.dv_packed_bytes(dv.Cache(dv.DV_PAGED, L, H, D, B, [0], elem_bytes=E,
+                                        block_size=bs, num_blocks=nb, max_blocks=maxb,
+                                        block_tables=[0]), l0, l1, t0, t1)
+        wire_h = synth.fill_bytes(n, 1000 + seed * 2 + call)
+        recv = G.dev_const(lay_b.storage_bytes(), 0xA5)
+        bt_b_dev = G.to_dev(bt_b)
+        rdesc = dv.Cache(dv.DV_PAGED, L, H, D, B, [recv], elem_bytes=E, block_size=bs,
+                         num_blocks=nb, max_blocks=maxb, block_tables=[bt_b_dev],
+                         block_owners=[ws])
+        wire = G.to_dev(wire_h)
+        if n:
+            dv.dv_stream_in(rdesc, 0, l0, l1, t0, t1, wire, n, stream())
+        torch.cuda.synchronize()
+        exp_recv = np.full(lay_b.storage_bytes(), 0xA5, np.uint8)
+        oracle_lib.unpack(lay_b, exp_recv, l0, l1, t0, t1, wire_h)
+        assert G.host(recv)[: lay_b.storage_bytes()].tobytes() == exp_recv.tobytes()
+        blocks = sum((t1[b] + bs - 1) // bs - t0[b] // bs for b in range(B) if t1[b] > t0[b])
+        pool_order = n > 0 and B <= 64 and (t1 - t0).max() > 1 and 2 * blocks >= nb
+        w = G.host(ws)
+        assert (w[nb * 4:] == 0x7E).all(), "wrote past the workspace"
+        if pool_order:
+            assert (w[: nb * 4].view(np.int32) ==
+                    G.owner_map_expected(bt_b, nb, bs, t0, t1)).all()
+        elif call == 0:
+            assert (w[: nb * 4] == 0x7E).all()
+
+
 @pytest.mark.parametrize("seed", range(8))
 def test_paged_token_increments(oracle_lib, seed):
     r = np.random.default_rng(300 + seed)

@@ -145,8 +145,9 @@ def test_llama_paged_gather_scatter_and_tail_increments(oracle_lib):
     bta, btb = G.to_dev(w.block_table_a), G.to_dev(w.block_table_b)
     ca = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool_a], block_size=bs, num_blocks=nb,
                   max_blocks=mbk, block_tables=[bta])
+    owners = G.dev_const(nb * 4, 0x7E)  # pool-order scatter, as the benchmark times it
     cb = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool_b], block_size=bs, num_blocks=nb,
-                  max_blocks=mbk, block_tables=[btb])
+                  max_blocks=mbk, block_tables=[btb], block_owners=[owners])
     t0, t1 = w.prompt_ranges()
     n = dv.dv_packed_bytes(ca, 0, L, t0, t1)
     wire = torch.empty(n, dtype=torch.uint8, device=G.DEV)
@@ -155,6 +156,8 @@ def test_llama_paged_gather_scatter_and_tail_increments(oracle_lib):
     G.check_pack_sampled(oracle_lib, la, w.data_seed, wire, 0, L, t0, t1, NSAMP, 5)
     dv.dv_stream_in(cb, 0, 0, L, t0, t1, wire, n, stream())
     torch.cuda.synchronize()
+    assert (G.host(owners).view(np.int32) ==
+            G.owner_map_expected(w.block_table_b, nb, bs, t0, t1)).all()
     # sampled: the scattered pool holds each sampled wire element where the
     # oracle's map through table B puts it
     rng = np.random.default_rng(6)
