@@ -119,7 +119,8 @@ struct CopyArgs {
 constexpr int kCopyUnroll = 2;
 
 constexpr int kKsplitTile = 64;
-constexpr int kKsplitMaxDu = 32;
+constexpr int kKsplitMaxDu = 32;  // LDS tile at most 64 x 33 units (33.8 KB)
+constexpr size_t kKsplitLdsFor4 = 39 * 1024;  // 4 per CU fit in 160 KB, 5 do not
 
 // Launchers (dv_kernels.hip).  Each returns the hipError_t of its launch.
 hipError_t launch_dense_runs(int dir, const DenseRunArgs& a, uint32_t tiles_per_slab,

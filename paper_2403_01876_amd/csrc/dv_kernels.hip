@@ -275,15 +275,19 @@ __global__ void __launch_bounds__(kThreads) token_kernel(TokenArgs a) {
 // Split-key slab: grid (tiles_per_slab, nslabs); a tile is 64 tokens of one
 // (sequence, head).  The cache holds the head as [group][token] (each group
 // 16 bytes), the wire as [token][group]: the tile is read with lanes along
-// the contiguous axis of the source, transposed through LDS, and written
-// with lanes along the contiguous axis of the destination.
+// the contiguous axis of the source, transposed through LDS (dynamic, 64
+// rows of du + 1 units: the padding unit keeps column accesses on distinct
+// banks), and written with lanes along the contiguous axis of the
+// destination.  Both passes take 4 units per lane at a time with clamped,
+// unguarded loads, so the loads of a pass issue back to back (a guarded load
+// per group left most of the load latency exposed: 70 % -> 77 % of HBM peak
+// on the OPT-13B shape).
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ void __launch_bounds__(kThreads) ksplit_kernel(KsplitArgs a) {
-  // one padding unit per row keeps the column accesses on distinct banks
-  __shared__ u32x4 tileL[kKsplitTile][kKsplitMaxDu + 1];
+  static_assert(kKsplitTile == 64, "cache-side units split as (group, token) = (j >> 6, j & 63)");
+  extern __shared__ u32x4 lds[];
   const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
   int n = 0, t0 = 0;
   if (lane < a.nseq) {
     n = a.r.n[lane];
@@ -306,9 +310,10 @@ __global__ void __launch_bounds__(kThreads) ksplit_kernel(KsplitArgs a) {
   const int r = tile - excl_b;
   const int h = r / tpr_b;
   const int k = r - h * tpr_b;
-  const int tok0 = k * kKsplitTile;                  // first token of the tile, range-relative
-  const int ntk = min(kKsplitTile, n_b - tok0);      // tokens in the tile
+  const int tok0 = k * kKsplitTile;              // first token of the tile, range-relative
+  const int ntk = min(kKsplitTile, n_b - tok0);  // tokens in the tile
   const int du = a.du;
+  const int pitch = du + 1;
 
   const int64_t slab = a.m.slab0 + y * a.m.slab_step;
   const int64_t wslab = a.m.wslab0 + y * a.m.slab_step;
@@ -317,23 +322,48 @@ __global__ void __launch_bounds__(kThreads) ksplit_kernel(KsplitArgs a) {
   u32x4* wire = (u32x4*)a.wire + wslab * a.m.w_slab + (int64_t)p_b * a.heads * du +
                 (int64_t)h * n_b * du + (int64_t)tok0 * du;
   const int64_t S = a.seq_cap;
-
+  // Cache side: unit j = group * 64 + token (tokens fastest); wire side:
+  // unit idx = token * du + group.
+  const int cache_units = du * kKsplitTile;
+  const int wire_units = ntk * du;
+  constexpr int kChunk = 4;
   if (D == kPack) {
-    for (int g = wave; g < du; g += kThreads / 64)
-      if (lane < ntk) tileL[lane][g] = ld_nt(head + g * S + lane);
+    for (int base = 0; base < cache_units; base += kChunk * kThreads) {
+      u32x4 v[kChunk];
+#pragma unroll
+      for (int i = 0; i < kChunk; ++i) {
+        const int j = min(base + i * kThreads + (int)threadIdx.x, cache_units - 1);
+        v[i] = ld_nt(head + (j >> 6) * S + min(j & 63, ntk - 1));
+      }
+#pragma unroll
+      for (int i = 0; i < kChunk; ++i) {
+        const int j = base + i * kThreads + (int)threadIdx.x;
+        if (j < cache_units && (j & 63) < ntk) lds[(j & 63) * pitch + (j >> 6)] = v[i];
+      }
+    }
     __syncthreads();
-    for (int idx = threadIdx.x; idx < ntk * du; idx += kThreads) {
-      const int t = idx / du, g = idx - t * du;
-      st_nt(tileL[t][g], wire + idx);
+    for (int idx = threadIdx.x; idx < wire_units; idx += kThreads) {
+      const int t = idx / du;
+      st_nt(lds[t * pitch + (idx - t * du)], wire + idx);
     }
   } else {
-    for (int idx = threadIdx.x; idx < ntk * du; idx += kThreads) {
-      const int t = idx / du, g = idx - t * du;
-      tileL[t][g] = ld_nt(wire + idx);
+    for (int base = 0; base < wire_units; base += kChunk * kThreads) {
+      u32x4 v[kChunk];
+#pragma unroll
+      for (int i = 0; i < kChunk; ++i)
+        v[i] = ld_nt(wire + min(base + i * kThreads + (int)threadIdx.x, wire_units - 1));
+#pragma unroll
+      for (int i = 0; i < kChunk; ++i) {
+        const int idx = base + i * kThreads + (int)threadIdx.x;
+        if (idx < wire_units) {
+          const int t = idx / du;
+          lds[t * pitch + (idx - t * du)] = v[i];
+        }
+      }
     }
     __syncthreads();
-    for (int g = wave; g < du; g += kThreads / 64)
-      if (lane < ntk) st_nt(tileL[lane][g], head + g * S + lane);
+    for (int j = threadIdx.x; j < cache_units; j += kThreads)
+      if ((j & 63) < ntk) st_nt(lds[(j & 63) * pitch + (j >> 6)], head + (j >> 6) * S + (j & 63));
   }
 }
 
@@ -394,10 +424,10 @@ namespace {
 // Launch with the runtime's own status for this launch (a stale error left by
 // an unrelated earlier call is not picked up, unlike hipGetLastError).
 template <typename Args>
-hipError_t launch(const void* fn, dim3 grid, const Args& a, hipStream_t s) {
+hipError_t launch(const void* fn, dim3 grid, const Args& a, hipStream_t s, size_t lds = 0) {
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
   void* args[] = {const_cast<Args*>(&a)};
-  return hipLaunchKernel(fn, grid, dim3(kThreads), args, 0, s);
+  return hipLaunchKernel(fn, grid, dim3(kThreads), args, lds, s);
 }
 
 }  // namespace
@@ -435,7 +465,12 @@ hipError_t launch_ksplit(int dir, const KsplitArgs& a, uint32_t tiles_per_slab, 
                          hipStream_t s) {
   const void* fn =
       dir == kPack ? (const void*)&ksplit_kernel<kPack> : (const void*)&ksplit_kernel<kUnpack>;
-  return launch(fn, dim3(tiles_per_slab, nslabs), a, s);
+  // The tile's LDS, rounded up for tiles of 16 KB or more so that at most 4
+  // workgroups share a CU's 160 KB: on MI355X 8 workgroups of 16 KB tiles
+  // ran 2-3 % slower than 4, while 8 KB tiles ran 13 % faster with 8.
+  size_t lds = (size_t)kKsplitTile * (a.du + 1) * sizeof(uint32_t) * 4;
+  if (a.du >= 16 && lds < kKsplitLdsFor4) lds = kKsplitLdsFor4;
+  return launch(fn, dim3(tiles_per_slab, nslabs), a, s, lds);
 }
 
 hipError_t launch_copy(const CopyArgs& a, uint32_t units_per_slab, uint32_t nslabs,

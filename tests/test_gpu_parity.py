@@ -259,7 +259,7 @@ def test_paged_token_increments(oracle_lib, seed):
     assert G.host(recv)[: lay.storage_bytes()].tobytes() == exp_recv.tobytes()
 
 
-@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("seed", range(24))
 def test_ksplit_pack_unpack(oracle_lib, seed):
     r = np.random.default_rng(400 + seed)
     L, H, D, B, S, E = rand_dense_shape(r)
@@ -287,6 +287,32 @@ def test_ksplit_pack_unpack(oracle_lib, seed):
     torch.cuda.synchronize()
     exp_recv = np.full(lay.storage_bytes(), 0xA5, np.uint8)
     oracle_lib.unpack(lay, exp_recv, l0, l1, t0, t1, wire_h)
+    assert G.host(recv)[: lay.storage_bytes()].tobytes() == exp_recv.tobytes()
+
+
+@pytest.mark.parametrize("D", [8, 32, 64, 128, 192, 256])
+def test_ksplit_group_counts(oracle_lib, D):
+    """Every count of 16-byte groups per token the split-key kernel takes in
+    one or several 4-unit passes (1 .. 32 groups; 16 and more get the padded
+    LDS request), with ragged 64-token tiles."""
+    r = np.random.default_rng(D)
+    L, H, B, S, E = 2, 3, 4, 150, 2
+    lay = oracle.Layout(oracle.KSPLIT, L, H, D, B, seq_cap=S, elem_bytes=E)
+    host_cache = synth.fill_bytes(lay.storage_bytes(), D + 1)
+    cache = G.to_dev(host_cache)  # the descriptor holds its address only
+    desc = dv.Cache(dv.DV_DENSE_KSPLIT, L, H, D, B, [cache], max_seq=S)
+    t0 = np.array([0, 5, 63, 0], np.int32)
+    t1 = np.array([150, 70, 64, int(r.integers(2, 150))], np.int32)
+    exp = oracle_lib.pack(lay, host_cache, 0, L, t0, t1)
+    assert run_pack(desc, 0, L, t0, t1, exp.nbytes).tobytes() == exp.tobytes()
+    wire_h = synth.fill_bytes(exp.nbytes, D + 2)
+    recv = G.dev_const(lay.storage_bytes(), 0xA5)
+    rdesc = dv.Cache(dv.DV_DENSE_KSPLIT, L, H, D, B, [recv], max_seq=S)
+    wire = G.to_dev(wire_h)
+    dv.dv_stream_in(rdesc, 0, 0, L, t0, t1, wire, exp.nbytes, stream())
+    torch.cuda.synchronize()
+    exp_recv = np.full(lay.storage_bytes(), 0xA5, np.uint8)
+    oracle_lib.unpack(lay, exp_recv, 0, L, t0, t1, wire_h)
     assert G.host(recv)[: lay.storage_bytes()].tobytes() == exp_recv.tobytes()
 
 
