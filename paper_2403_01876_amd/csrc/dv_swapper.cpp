@@ -76,6 +76,8 @@ int dv_swapper_create(const dv_cache* dev_slots, const dv_cache* host, dv_swappe
   s->dev.num_mb = 2;
   s->dev.mb_base = s->dev_base.data();
   s->host.mb_base = s->host_base.data();
+  s->dev.block_table = s->host.block_table = nullptr;  // dense: never read
+  s->dev.block_owner = s->host.block_owner = nullptr;
   s->slot_of.assign(host->num_mb, -1);
   // Streams at the default priority.
   if (hipStreamCreateWithFlags(&s->s_in, hipStreamNonBlocking) != hipSuccess ||
