@@ -240,7 +240,8 @@ def increments_bench(torch, dv, synth):
         torch.cuda.synchronize()
         graph_us = a.elapsed_time(b) / n * 1e3
         out[w.name] = {
-            "bytes": I, "eager_us_per_call": round(eager_us, 3),
+            "bytes": I, "cache_state": "warm (back-to-back calls)",
+            "eager_us_per_call": round(eager_us, 3),
             "graph_us_per_call": round(graph_us, 3),
             "eager_GBps_2x": round(2 * I / (eager_us * 1e-6) / 1e9, 1),
             "graph_GBps_2x": round(2 * I / (graph_us * 1e-6) / 1e9, 1),
@@ -321,10 +322,59 @@ def bulk_bench(torch, dv, synth, idx, reps=10, ksplit=False):
         ms = t.mean_ms()
         gbs = 2 * P / (ms * 1e-3) / 1e9
         res[name] = {"ms": round(ms, 4), "min_ms": round(t.min_ms(), 4),
-                     "GBps_2x": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
+                     "GBps_2x": round(gbs, 1), "payload_GBps": round(gbs / 2, 1),
+                     "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
+    res["cache_state"] = "cold: 512 MB written between calls"
     del a, r, wire, scratch
     torch.cuda.empty_cache()
     return w, res
+
+
+def tiny_bench(torch, dv, synth, reps=20):
+    """The tiny correctness workload (2 layers, 4 heads x 64, batch 2, prompts of
+    100): prompt stream-out / stream-in and 16 increments, cold (512 MB
+    written before each call) and warm (back to back).  Latency-bound: a
+    fraction of HBM peak means nothing at 409 600 bytes."""
+    dev = torch.device("cuda:0")
+    w = synth.make_workload(0)
+    L, H, D, B, S = w.layers, w.heads, w.head_dim, w.batch, w.max_seq
+    stream = torch.cuda.current_stream()
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    a = torch.empty(w.dense_bytes(), dtype=torch.uint8, device=dev)
+    r = torch.zeros_like(a)
+    synth.device_fill(a.data_ptr(), a.numel(), w.data_seed, stream=stream.cuda_stream)
+    ca = dv.Cache(dv.DV_DENSE, L, H, D, B, [a], max_seq=S)
+    cr = dv.Cache(dv.DV_DENSE, L, H, D, B, [r], max_seq=S)
+    t0, t1 = w.prompt_ranges()
+    P = dv.dv_packed_bytes(ca, 0, L, t0, t1)
+    wire = torch.empty(P, dtype=torch.uint8, device=dev)
+    p = w.step_positions(0)
+    I = dv.dv_packed_bytes(ca, 0, L, p, p + 1)
+    inc = torch.empty(I, dtype=torch.uint8, device=dev)
+    ops = {
+        "prompt_out": lambda: dv.dv_stream_out_prompt(ca, 0, 0, L, t0, t1, wire, P, stream),
+        "prompt_in": lambda: dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, P, stream),
+        "increment_out": lambda: dv.dv_stream_out_token(ca, 0, 0, L, p, inc, I, stream),
+        "increment_in": lambda: dv.dv_stream_in(cr, 0, 0, L, p, p + 1, inc, I, stream),
+    }
+    res = {"payload_prompt_bytes": P, "payload_increment_bytes": I,
+           "note": "latency-bound; % of HBM peak not meaningful"}
+    for name, op in ops.items():
+        op()
+        cold, warm = Timer(torch, stream), Timer(torch, stream)
+        for _ in range(reps):
+            flush_l2(torch, scratch)
+            with cold:
+                op()
+        for _ in range(reps):
+            with warm:
+                op()
+        torch.cuda.synchronize()
+        res[name] = {"cold_us": round(cold.mean_ms() * 1e3, 2),
+                     "warm_us": round(warm.mean_ms() * 1e3, 2)}
+    del scratch, a, r, wire, inc
+    torch.cuda.empty_cache()
+    return res
 
 
 def swap_bench(torch, dv, synth, reps=3):
@@ -379,6 +429,37 @@ def swap_bench(torch, dv, synth, reps=3):
     res["bidirectional"] = {"ms": round(bi_ms, 3),
                             "GBps_total": round(2 * P / (bi_ms * 1e-3) / 1e9, 2)}
     del t_start
+    # decode-step increment packs on the compute stream, idle and while both
+    # swap directions run on their own streams (slot 0 is read by both the
+    # packs and the swap-out; the swap-in writes slot 1)
+    comp = torch.cuda.current_stream()
+    I = dv.dv_packed_bytes(ds, 0, L, lens, lens + 1)
+    inc = torch.empty(I, dtype=torch.uint8, device=dev)
+    n_inc = 200
+
+    def time_incs():
+        t = Timer(torch, comp)
+        with t:
+            for _ in range(n_inc):
+                dv.dv_stream_out_token(ds, 0, 0, L, lens, inc, I, comp)
+        return t
+
+    time_incs()
+    torch.cuda.synchronize()
+    idle = time_incs()
+    torch.cuda.synchronize()
+    dv.dv_swap_in(hh, 1, ds, 1, 0, L, zero, lens, s_in)
+    dv.dv_swap_out(ds, 0, hh, 0, 0, L, zero, lens, s_out)
+    busy = time_incs()
+    comp.synchronize()
+    still_running = not s_in.query()
+    torch.cuda.synchronize()
+    res["increments_under_swap"] = {
+        "increment_bytes": I, "calls": n_inc,
+        "idle_us_per_call": round(idle.mean_ms() * 1e3 / n_inc, 3),
+        "during_swaps_us_per_call": round(busy.mean_ms() * 1e3 / n_inc, 3),
+        "swaps_still_running_after_packs": still_running,
+    }
     # host-link calibration: one contiguous copy of the same byte count
     flat_d = slots[0][:P]
     flat_h = hosts[0][:P]
@@ -907,8 +988,10 @@ def main():
     if extras == "all":
         log("extras: increments")
         out["increments"] = increments_bench(torch, dv, synth)
+        log("extras: tiny workload")
+        out["tiny"] = tiny_bench(torch, dv, synth)
         log("extras: bulk workloads")
-        for idx in (3, 4):
+        for idx in (2, 3, 4):
             wk, res = bulk_bench(torch, dv, synth, idx)
             out.setdefault("bulk", {})[wk.name] = res
         wk, res = bulk_bench(torch, dv, synth, 1, ksplit=True)
