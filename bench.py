@@ -747,6 +747,12 @@ def overlap_bench(torch, dv, synth):
                                              base["token_ms_per_step"] - 1, 4)
     out["token_slowdown_inline"] = round(inl["token_ms_per_step"] /
                                          base["token_ms_per_step"] - 1, 4)
+    # share of the streaming time (what inline streaming adds) that the
+    # background streamer hides behind the computation
+    for ph, key in (("prompt", "prompt_ms"), ("token", "token_ms_per_step")):
+        added = inl[key] - base[key]
+        out[f"{ph}_hidden_fraction"] = (round(1 - (ov[key] - base[key]) / added, 4)
+                                        if added > 0 else None)
     del cache, staging, host, Wt, Xp, Xt
     torch.cuda.empty_cache()
     return out
@@ -803,6 +809,17 @@ def ring_recovery_bench(torch, dv, synth):
            "recovery_GBps_2x": round(2 * moved / (rec_ms * 1e-3) / 1e9, 1)}
     del sim
     torch.cuda.empty_cache()
+    return out
+
+
+def device_facts(torch):
+    """What the runtime reports about the GPU the numbers come from."""
+    p = torch.cuda.get_device_properties(0)
+    out = {"name": p.name, "compute_units": p.multi_processor_count,
+           "hbm_bytes": p.total_memory}
+    for k in ("gcnArchName", "L2_cache_size", "shared_memory_per_block"):
+        if hasattr(p, k):
+            out[k] = getattr(p, k)
     return out
 
 
@@ -953,6 +970,7 @@ def main():
         "vs_baseline": None,
         "dtype": "u16",
         "data": "synthetic",
+        "device": device_facts(torch),
         "config": {
             "workload": ("opt13b-stage: 10 layers x 40 heads x 128 dims, batch 8, capacity "
                          "2048, fp16 dense [layer][K|V][batch][head][seq][dim], prompts "

@@ -18,8 +18,12 @@
  *
  * Conventions shared by every call:
  *  - Return value: DV_OK (0) or a negative dv_status.  Arguments are checked
- *    on the host before anything is enqueued; on any error nothing is
- *    enqueued and no memory is touched.
+ *    on the host before anything is enqueued; on a validation error
+ *    (DV_ERR_INVALID, _RANGE, _SPACE, _UNSUPPORTED) nothing is enqueued and no
+ *    memory is touched.  DV_ERR_HIP means the runtime refused a launch or
+ *    copy; a call that enqueues several (more than 64 sequences, split-key
+ *    caches, ragged swaps, owner maps) may then have enqueued the ones
+ *    before it, so the destination is unspecified until the call succeeds.
  *  - Asynchrony: work is enqueued on `stream` (a hipStream_t; NULL is the
  *    null stream) and is complete only once that stream has been
  *    synchronised.  Host arrays passed in (ranges, mb_base, block_table) are

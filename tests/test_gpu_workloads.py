@@ -98,6 +98,58 @@ def test_opt13b_stage_prompt_and_increments(oracle_lib):
                                 sentinel=0xA5)
 
 
+def test_opt13b_stage_split_key_full_size(oracle_lib):
+    """The OPT-13B stage stored with the split-key layout, as the benchmark
+    times it: sampled pack against the oracle, then stream-in into a sentinel
+    receiver checked over every byte through full-capacity re-packs (a
+    [0, max_seq) stream of any layout is the dense [layer][K|V][seq][head]
+    [token][dim] order)."""
+    w = synth.make_workload(1)
+    L, H, D, B, S, E = w.layers, w.heads, w.head_dim, w.batch, w.max_seq, w.elem_bytes
+    lay = oracle.Layout(oracle.KSPLIT, L, H, D, B, seq_cap=S, elem_bytes=E)
+    cache = G.dev_filled(lay.storage_bytes(), w.data_seed)
+    cs = dv.Cache(dv.DV_DENSE_KSPLIT, L, H, D, B, [cache], max_seq=S)
+    t0, t1 = w.prompt_ranges()
+    n = dv.dv_packed_bytes(cs, 0, L, t0, t1)
+    wire = torch.empty(n, dtype=torch.uint8, device=G.DEV)
+    dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, n, stream())
+    torch.cuda.synchronize()
+    G.check_pack_sampled(oracle_lib, lay, w.data_seed, wire, 0, L, t0, t1, NSAMP, 11)
+    recv = G.dev_const(lay.storage_bytes(), 0xA5)
+    cr = dv.Cache(dv.DV_DENSE_KSPLIT, L, H, D, B, [recv], max_seq=S)
+    dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, n, stream())
+    zero, full = np.zeros(B, np.int32), np.full(B, S, np.int32)
+    m = dv.dv_packed_bytes(cs, 0, L, zero, full)
+    src_d = torch.empty(m, dtype=torch.uint8, device=G.DEV)
+    recv_d = torch.empty(m, dtype=torch.uint8, device=G.DEV)
+    dv.dv_stream_out_prompt(cs, 0, 0, L, zero, full, src_d, m, stream())
+    dv.dv_stream_out_prompt(cr, 0, 0, L, zero, full, recv_d, m, stream())
+    torch.cuda.synchronize()
+    G.assert_dense_ranges_equal(recv_d, src_d, L, B, H, S, D, E, 0, L, t0, t1, sentinel=0xA5)
+
+
+def test_opt66b_microbatch_prompt_full_size(oracle_lib):
+    """One OPT-66B stage microbatch (4.7 GB payload) streamed out and in, as
+    the benchmark's bulk measurement times it."""
+    w = synth.make_workload(2)
+    lay, L, H, D, B, S = dense_pair(w)
+    E = w.elem_bytes
+    cache = G.dev_filled(lay.storage_bytes(), w.data_seed)
+    cs = dv.Cache(dv.DV_DENSE, L, H, D, B, [cache], max_seq=S)
+    t0, t1 = w.prompt_ranges()
+    n = dv.dv_packed_bytes(cs, 0, L, t0, t1)
+    assert n == 4718592000
+    wire = torch.empty(n, dtype=torch.uint8, device=G.DEV)
+    dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, n, stream())
+    torch.cuda.synchronize()
+    G.check_pack_sampled(oracle_lib, lay, w.data_seed, wire, 0, L, t0, t1, NSAMP, 12)
+    recv = G.dev_const(lay.storage_bytes(), 0xA5)
+    cr = dv.Cache(dv.DV_DENSE, L, H, D, B, [recv], max_seq=S)
+    dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, n, stream())
+    torch.cuda.synchronize()
+    G.assert_dense_ranges_equal(recv, cache, L, B, H, S, D, E, 0, L, t0, t1, sentinel=0xA5)
+
+
 def test_bloom_shard_replicate_and_restore(oracle_lib):
     """Full valid cache -> contiguous replica; poison; restore from the replica."""
     w = synth.make_workload(3)
