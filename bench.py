@@ -61,8 +61,9 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-extras", action="store_true")
-    p.add_argument("--extras", choices=("all", "calib", "none"), default="all",
-                   help="calib: only the known-size copy used to scale counter runs")
+    p.add_argument("--extras", choices=("all", "bulk", "calib", "none"), default="all",
+                   help="calib: only the known-size copy used to scale counter runs; "
+                        "bulk: the bulk workloads and that copy")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--eager", action="store_true",
                    help="report the step issued call by call instead of graph-replayed")
@@ -375,6 +376,19 @@ def tiny_bench(torch, dv, synth, reps=20):
     del scratch, a, r, wire, inc
     torch.cuda.empty_cache()
     return res
+
+
+def bulk_all(torch, dv, synth):
+    """Bulk stream-out / stream-in of the OPT-66B microbatch, the BLOOM shard,
+    the LLaMA paged pool and the split-key OPT-13B stage."""
+    log("extras: bulk workloads")
+    out = {}
+    for idx in (2, 3, 4):
+        wk, res = bulk_bench(torch, dv, synth, idx)
+        out[wk.name] = res
+    wk, res = bulk_bench(torch, dv, synth, 1, ksplit=True)
+    out[wk.name + " split-key"] = res
+    return out
 
 
 def swap_bench(torch, dv, synth, reps=3):
@@ -1003,17 +1017,15 @@ def main():
     extras = "none" if args.no_extras else args.extras
     if extras == "calib":
         out["calibration_d2d_copy"] = copy_calibration(torch)
+    if extras == "bulk":
+        out["bulk"] = bulk_all(torch, dv, synth)
+        out["calibration_d2d_copy"] = copy_calibration(torch)
     if extras == "all":
         log("extras: increments")
         out["increments"] = increments_bench(torch, dv, synth)
         log("extras: tiny workload")
         out["tiny"] = tiny_bench(torch, dv, synth)
-        log("extras: bulk workloads")
-        for idx in (2, 3, 4):
-            wk, res = bulk_bench(torch, dv, synth, idx)
-            out.setdefault("bulk", {})[wk.name] = res
-        wk, res = bulk_bench(torch, dv, synth, 1, ksplit=True)
-        out["bulk"][wk.name + " split-key"] = res
+        out["bulk"] = bulk_all(torch, dv, synth)
         log("extras: swap")
         out["swap"] = swap_bench(torch, dv, synth)
         log("extras: swap protocol")
