@@ -42,7 +42,8 @@ struct View {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-int view_of(const dv_cache* c, int32_t mb, View* v) {
+// The layout of a descriptor, without a microbatch (sizing calls).
+int layout_of(const dv_cache* c, View* v) {
   if (!c || !c->mb_base) return DV_ERR_INVALID;
   if (c->elem_bytes <= 0 || c->num_layers <= 0 || c->num_heads <= 0 || c->head_dim <= 0 ||
       c->batch <= 0 || c->num_mb <= 0)
@@ -79,11 +80,15 @@ int view_of(const dv_cache* c, int32_t mb, View* v) {
   if (v->cap > (1 << 24) || v->du > (1 << 16) || v->H * v->du > (1 << 20) ||
       v->cap * v->du > (1ll << 30))
     return DV_ERR_UNSUPPORTED;
-  if (mb < 0) {  // sizing only, no microbatch
-    v->base = nullptr;
-    return DV_OK;
-  }
-  if (mb >= c->num_mb) return DV_ERR_RANGE;
+  v->base = nullptr;
+  return DV_OK;
+}
+
+// The layout plus microbatch mb's base address (and table, owner map).
+int view_of(const dv_cache* c, int32_t mb, View* v) {
+  const int rc = layout_of(c, v);
+  if (rc != DV_OK) return rc;
+  if (mb < 0 || mb >= c->num_mb) return DV_ERR_RANGE;
   v->base = static_cast<char*>(c->mb_base[mb]);
   if (!v->base || !aligned16(v->base)) return DV_ERR_INVALID;
   if (c->kind == DV_PAGED) {
@@ -448,7 +453,7 @@ const char* dv_status_string(int status) {
 
 int dv_cache_bytes(const dv_cache* c, uint64_t* out_bytes) {
   View v;
-  int rc = view_of(c, -1, &v);
+  int rc = layout_of(c, &v);
   if (rc != DV_OK) return rc;
   if (out_bytes) *out_bytes = v.bytes;
   return DV_OK;
@@ -457,7 +462,7 @@ int dv_cache_bytes(const dv_cache* c, uint64_t* out_bytes) {
 int dv_packed_bytes(const dv_cache* c, int32_t l0, int32_t l1, const int32_t* t0,
                     const int32_t* t1, uint64_t* out_bytes) {
   View v;
-  int rc = view_of(c, -1, &v);
+  int rc = layout_of(c, &v);
   if (rc != DV_OK) return rc;
   std::vector<int32_t> r0, rn;
   int64_t N = 0;

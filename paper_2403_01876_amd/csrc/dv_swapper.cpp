@@ -48,6 +48,14 @@ void release(dv_swapper* s) {
   delete s;
 }
 
+// The ranges [t0, t1) fit both the device slots and the host mirrors, so
+// the swap calls of a step can only fail in the runtime.
+int check_ranges(const dv_swapper* s, const int32_t* t0, const int32_t* t1) {
+  int rc = dv_packed_bytes(&s->dev, 0, s->dev.num_layers, t0, t1, nullptr);
+  if (rc == DV_OK) rc = dv_packed_bytes(&s->host, 0, s->host.num_layers, t0, t1, nullptr);
+  return rc;
+}
+
 }  // namespace
 
 extern "C" {
@@ -113,14 +121,16 @@ int dv_swapper_prefetch(dv_swapper* s, int32_t mb, const int32_t* len) {
   const int slot = s->next_slot;
   const int prev = s->occupant[slot];
   if (!s->done[slot]) return DV_ERR_INVALID;  // occupant's step has not ended
-  if (prev >= 0) s->slot_of[prev] = -1;
+  int rc = check_ranges(s, nullptr, len);
+  if (rc != DV_OK) return rc;
   // The slot is reused only after its previous occupant's update has left.
   if (prev >= 0 && hipStreamWaitEvent(s->s_in, s->freed[slot], 0) != hipSuccess)
     return DV_ERR_HIP;
-  int rc = dv_swap_in(&s->host, mb, &s->dev, slot, 0, s->host.num_layers, nullptr, len, s->s_in);
+  rc = dv_swap_in(&s->host, mb, &s->dev, slot, 0, s->host.num_layers, nullptr, len, s->s_in);
   if (rc != DV_OK) return rc;
   rc = hip_ok(hipEventRecord(s->resident[slot], s->s_in));
   if (rc != DV_OK) return rc;
+  if (prev >= 0) s->slot_of[prev] = -1;
   s->occupant[slot] = mb;
   s->slot_of[mb] = slot;
   s->done[slot] = false;
@@ -146,7 +156,9 @@ int dv_swapper_end_step(dv_swapper* s, int32_t mb, void* compute_stream, const i
   if (mb < 0 || mb >= s->host.num_mb) return DV_ERR_RANGE;
   const int slot = s->slot_of[mb];
   if (slot < 0) return DV_ERR_RANGE;
-  int rc = hip_ok(hipEventRecord(s->step_done, static_cast<hipStream_t>(compute_stream)));
+  int rc = check_ranges(s, t0, t1);
+  if (rc != DV_OK) return rc;
+  rc = hip_ok(hipEventRecord(s->step_done, static_cast<hipStream_t>(compute_stream)));
   if (rc != DV_OK) return rc;
   if (hipStreamWaitEvent(s->s_out, s->step_done, 0) != hipSuccess) return DV_ERR_HIP;
   rc = dv_swap_out(&s->dev, slot, &s->host, mb, 0, s->host.num_layers, t0, t1, s->s_out);

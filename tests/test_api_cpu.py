@@ -72,6 +72,31 @@ def test_packed_bytes_paged():
     del bt
 
 
+def test_negative_microbatch_and_slot_are_rejected():
+    """Every call that addresses a microbatch or slot rejects an index below
+    zero with DV_ERR_RANGE before touching memory (a regression test: an
+    index of -1 once reached the sizing-only path and passed a null base)."""
+    c = dense(bases=(FAKE, FAKE + (1 << 32)))
+    h = dense(bases=(FAKE + (1 << 34),), mem=dv.DV_MEM_HOST_PINNED)
+    z = np.zeros(4, np.int32)
+    t1 = np.full(4, 10, np.int32)
+    wire = FAKE + (1 << 36)
+    for mb in (-1, -2, 2):
+        rc, _ = dv.dv_stream_out_prompt(c, mb, 0, 2, z, t1, wire, 1 << 30, check=False)
+        assert rc == dv.DV_ERR_RANGE, mb
+        rc, _ = dv.dv_stream_out_token(c, mb, 0, 2, t1, wire, 1 << 30, check=False)
+        assert rc == dv.DV_ERR_RANGE, mb
+        assert dv.dv_stream_in(c, mb, 0, 2, z, t1, wire, 1 << 30, check=False) == dv.DV_ERR_RANGE
+        assert dv.dv_swap_out(c, mb, h, 0, 0, 2, z, t1, check=False) == dv.DV_ERR_RANGE
+        assert dv.dv_swap_in(h, 0, c, mb, 0, 2, z, t1, check=False) == dv.DV_ERR_RANGE
+    for hb in (-1, 1):
+        assert dv.dv_swap_out(c, 0, h, hb, 0, 2, z, t1, check=False) == dv.DV_ERR_RANGE
+        assert dv.dv_swap_in(h, hb, c, 0, 0, 2, z, t1, check=False) == dv.DV_ERR_RANGE
+    # sizing calls take no microbatch and still work
+    assert dv.dv_packed_bytes(c, 0, 2, z, t1) == 2 * 2 * 3 * 64 * 2 * 40
+    assert dv.dv_cache_bytes(c) == 2 * 2 * 4 * 3 * 50 * 64 * 2
+
+
 def test_owner_workspace_rejections():
     """A paged receiver's owner-map workspace must be 4-byte aligned and must
     not overlap the pool or the source buffer; all checked on the host."""

@@ -275,3 +275,31 @@ def test_swapper_refuses_refill_before_step_end():
     assert sw.prefetch(2, lens) == dv.DV_OK  # slot 0 is free again
     sw.sync()
     sw.close()
+
+
+def test_swapper_rejects_bad_ranges_without_changing_state():
+    """A prefetch or end_step whose ranges do not fit the slots or the host
+    mirrors is refused before anything is enqueued, and the scheduler's
+    state is as before: the same calls with good ranges then work."""
+    L, H, D, B = 1, 1, 64, 2
+    S, S_host = 16, 8
+    slots = [G.dev_const(L * 2 * B * H * S * D * 2, 0) for _ in range(2)]
+    hosts = [pinned(L * 2 * B * H * S_host * D * 2, 0) for _ in range(3)]
+    ds = dv.Cache(dv.DV_DENSE, L, H, D, B, slots, max_seq=S)
+    hh = dv.Cache(dv.DV_DENSE, L, H, D, B, [t.data_ptr() for t in hosts], max_seq=S_host,
+                  mem=dv.DV_MEM_HOST_PINNED)
+    sw = dv.Swapper(ds, hh)
+    good = np.array([4, 5], np.int32)
+    for bad in (np.array([9, 1], np.int32), np.array([-1, 1], np.int32)):
+        assert sw.prefetch(0, bad, check=False) == dv.DV_ERR_RANGE  # 9 > host capacity 8
+    assert sw.prefetch(0, good) == dv.DV_OK
+    assert sw.prefetch(1, good) == dv.DV_OK
+    assert sw.begin_step(0) == 0
+    assert sw.end_step(0, [4, 5], [9, 6], check=False) == dv.DV_ERR_RANGE
+    assert sw.end_step(0, [5, 4], [4, 5], check=False) == dv.DV_ERR_RANGE  # t1 < t0
+    # the refused end_step did not free slot 0
+    assert sw.prefetch(2, good, check=False) == dv.DV_ERR_INVALID
+    assert sw.end_step(0, [4, 5], [5, 6]) == dv.DV_OK
+    assert sw.prefetch(2, good) == dv.DV_OK
+    sw.sync()
+    sw.close()
