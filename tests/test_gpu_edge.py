@@ -183,6 +183,85 @@ def test_paged_unmapped_entries_are_skipped(oracle_lib):
             assert G.host(ws).view(np.int32).tolist() == [0, 1, 2, 3, 5, 6, 8]
 
 
+def test_graph_replay_paged_pool_order_and_split_key(oracle_lib):
+    """Captured: a paged gather, a pool-order scatter (owner map rebuilt by
+    kernels inside the graph), tail-block increments, and a split-key
+    round trip.  Each replay starts from a sentinel receiver and a garbage
+    owner workspace and must give the oracle's result."""
+    L, H, D, B, bs = 2, 3, 128, 5, 16
+    lens = [40, 17, 64, 1, 33]
+    steps = 4
+    maxb = max((n + steps + bs - 1) // bs for n in lens) + 1
+    bt, nb = synth.make_paged_tables(77, [n + steps for n in lens], bs, maxb)
+    valid = bt >= 0
+    bt_b = bt.copy()
+    bt_b[valid] = np.random.default_rng(3).permutation(bt[valid])
+    la = oracle.Layout(oracle.PAGED, L, H, D, B, block_size=bs, num_blocks=nb, block_table=bt)
+    lb = oracle.Layout(oracle.PAGED, L, H, D, B, block_size=bs, num_blocks=nb, block_table=bt_b)
+    host = synth.fill_bytes(la.storage_bytes(), 78)
+    pool_a = G.to_dev(host)
+    pool_b = G.dev_const(lb.storage_bytes(), 0)
+    owners = G.dev_const(nb * 4, 0x7E)
+    bta, btb = G.to_dev(bt), G.to_dev(bt_b)
+    ca = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool_a], block_size=bs, num_blocks=nb,
+                  max_blocks=maxb, block_tables=[bta])
+    cb = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool_b], block_size=bs, num_blocks=nb,
+                  max_blocks=maxb, block_tables=[btb], block_owners=[owners])
+    t0 = np.zeros(B, np.int32)
+    t1 = np.array(lens, np.int32)
+    P = dv.dv_packed_bytes(ca, 0, L, t0, t1)
+    wire = G.dev_const(P, 0)
+    I = dv.dv_packed_bytes(ca, 0, L, t1, t1 + 1)
+    inc = G.dev_const(I, 0)
+    S = 96
+    kl = oracle.Layout(oracle.KSPLIT, L, H, D, B, seq_cap=S)
+    khost = synth.fill_bytes(kl.storage_bytes(), 79)
+    ks = G.to_dev(khost)
+    kr = G.dev_const(kl.storage_bytes(), 0)
+    ck = dv.Cache(dv.DV_DENSE_KSPLIT, L, H, D, B, [ks], max_seq=S)
+    ckr = dv.Cache(dv.DV_DENSE_KSPLIT, L, H, D, B, [kr], max_seq=S)
+    kt1 = np.minimum(t1, S).astype(np.int32)
+    KP = dv.dv_packed_bytes(ck, 0, L, t0, kt1)
+    kwire = G.dev_const(KP, 0)
+
+    def step(st):
+        dv.dv_stream_out_prompt(ca, 0, 0, L, t0, t1, wire, P, st)
+        dv.dv_stream_in(cb, 0, 0, L, t0, t1, wire, P, st)
+        for i in range(steps):
+            p = t1 + i
+            dv.dv_stream_out_token(ca, 0, 0, L, p, inc, I, st)
+            dv.dv_stream_in(cb, 0, 0, L, p, p + 1, inc, I, st)
+        dv.dv_stream_out_prompt(ck, 0, 0, L, t0, kt1, kwire, KP, st)
+        dv.dv_stream_in(ckr, 0, 0, L, t0, kt1, kwire, KP, st)
+
+    exp_b = np.full(lb.storage_bytes(), 0xA5, np.uint8)
+    oracle_lib.unpack(lb, exp_b, 0, L, t0, t1, oracle_lib.pack(la, host, 0, L, t0, t1))
+    for i in range(steps):
+        p = t1 + i
+        oracle_lib.unpack(lb, exp_b, 0, L, p, p + 1, oracle_lib.pack(la, host, 0, L, p, p + 1))
+    exp_k = np.full(kl.storage_bytes(), 0x3C, np.uint8)
+    oracle_lib.unpack(kl, exp_k, 0, L, t0, kt1, oracle_lib.pack(kl, khost, 0, L, t0, kt1))
+
+    side = torch.cuda.Stream()
+    side.wait_stream(stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            step(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    for rep in range(4):
+        pool_b.fill_(0xA5)
+        owners.fill_(0x40 + rep)
+        kr.fill_(0x3C)
+        wire.fill_(rep)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert G.host(pool_b).tobytes() == exp_b.tobytes(), rep
+        assert G.host(kr).tobytes() == exp_k.tobytes(), rep
+        assert (G.host(owners).view(np.int32) == G.owner_map_expected(bt_b, nb, bs, t0, t1)).all()
+
+
 def test_graph_replay_matches_eager(oracle_lib):
     """A captured step replayed several times, with eager work and syncs in
     between, gives the eager result every time."""
