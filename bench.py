@@ -100,6 +100,22 @@ def flush_l2(torch, scratch):
     scratch.add_(1)
 
 
+def ranges_match(torch, recv, src, L, B, H, S, D, t0, t1, fill=0):
+    """Receiver equals source on the token ranges of every (layer, K|V,
+    sequence, head) of two dense fp16 caches, and holds `fill` bytes
+    everywhere else (the streaming invariants, checked on the device)."""
+    r = recv[: L * 2 * B * H * S * D * 2].view(torch.int16).view(L, 2, B, H, S, D)
+    x = src[: L * 2 * B * H * S * D * 2].view(torch.int16).view(L, 2, B, H, S, D)
+    outside = torch.ones((L, 2, B, H, S), dtype=torch.bool, device=recv.device)
+    for b in range(B):
+        a, e = int(t0[b]), int(t1[b])
+        if not torch.equal(r[:, :, b, :, a:e], x[:, :, b, :, a:e]):
+            return False
+        outside[:, :, b, :, a:e] = False
+    fv = torch.tensor([fill], dtype=torch.uint8, device=recv.device).repeat(2).view(torch.int16)
+    return bool((r[outside] == fv).all())
+
+
 def main_step_bench(args, torch, dv, synth):
     """The step on the OPT-13B stage: replayed as one captured HIP graph (the
     default; the 258 launches of a step are launch-bound otherwise) or issued
@@ -152,6 +168,12 @@ def main_step_bench(args, torch, dv, synth):
         step(stream)
     eager_ms = timed(lambda: step(stream), args.steps)
     log(f"eager: {eager_ms:.3f} ms/step")
+    # The step's own invariants (no oracle): the receiver, zero before,
+    # equals the sender on [0, len + steps) and is zero elsewhere.
+    full = t1 + w.steps
+    checks = {"eager_receiver_equals_sender_on_ranges":
+              ranges_match(torch, recv, sender, L, B, H, S, D, t0, full)}
+    eager_wire = wire.clone()
     # graph
     side = torch.cuda.Stream()
     side.wait_stream(stream)
@@ -164,6 +186,14 @@ def main_step_bench(args, torch, dv, synth):
         graph.replay()
     graph_ms = timed(graph.replay, args.steps)
     log(f"graph: {graph_ms:.3f} ms/step")
+    recv.zero_()
+    wire.zero_()
+    graph.replay()
+    torch.cuda.synchronize()
+    checks["graph_receiver_equals_sender_on_ranges"] = ranges_match(
+        torch, recv, sender, L, B, H, S, D, t0, full)
+    checks["graph_wire_equals_eager_wire"] = bool(torch.equal(wire, eager_wire))
+    del eager_wire
     ms = eager_ms if args.eager else graph_ms
 
     # Per-kernel durations: one event pair around back-to-back launches that
@@ -184,7 +214,7 @@ def main_step_bench(args, torch, dv, synth):
     res = {
         "ms": ms, "eager_ms": eager_ms, "graph_ms": graph_ms, "P": P, "I": I,
         "step_bytes": step_bytes, "value": step_bytes / (ms * 1e-3) / 1e9,
-        "pack_ms": kern["pack"], "unpack_ms": kern["unpack"],
+        "pack_ms": kern["pack"], "unpack_ms": kern["unpack"], "checks": checks,
     }
     del sender, recv, wire, incs, graph
     torch.cuda.empty_cache()
@@ -316,6 +346,18 @@ def bulk_bench(torch, dv, synth, idx, reps=10, ksplit=False):
                 dv.dv_stream_in(cr_table, 0, 0, L, t0, t1, wire, P, stream)
     torch.cuda.synchronize()
     res = {"payload_bytes": P}
+    # invariants after timing: the receiver holds the sender's ranges (dense:
+    # directly; paged and split key: re-packed, since a stream of any layout
+    # is in one canonical order)
+    if w.paged or ksplit:
+        again = torch.empty_like(wire)
+        dv.dv_stream_out_prompt(cr, 0, 0, L, t0, t1, again, P, stream)
+        torch.cuda.synchronize()
+        res["check_receiver_repacks_to_wire"] = bool(torch.equal(again, wire))
+        del again
+    else:
+        res["check_receiver_equals_sender_on_ranges"] = ranges_match(
+            torch, r, a, L, B, H, w.max_seq, D, t0, t1)
     timers = [("stream_out", tp), ("stream_in", tu)]
     if w.paged:
         timers.append(("stream_in_table_order", tt))
@@ -996,6 +1038,7 @@ def main():
             "step_issue": "eager" if args.eager else "hip graph replay",
             "eager_ms_per_step": round(r["eager_ms"], 4),
             "graph_ms_per_step": round(r["graph_ms"], 4),
+            "checks": r["checks"],
         },
         "roofline": {
             "kernel": "dense_runs_kernel<pack> (prompt stream-out)",
@@ -1043,6 +1086,12 @@ def main():
         log("cpu baseline (oracle)")
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out), flush=True)
+    failed = [k for k, v in r["checks"].items() if not v]
+    for name, res in out.get("bulk", {}).items():
+        failed += [f"{name}: {k}" for k, v in res.items() if k.startswith("check_") and not v]
+    if failed:
+        log("invariant checks failed, numbers invalid: " + ", ".join(failed))
+        sys.exit(1)
 
 
 if __name__ == "__main__":
