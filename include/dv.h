@@ -262,8 +262,9 @@ DV_API int dv_swapper_destroy(dv_swapper* s);
  * contiguous buffer in `dst`, since layer ranges concatenate; decode steps
  * can cycle through a few staging slots while filling a long host log.
  * Pushes run in push order.  `staging` (device) and `dst` are caller owned,
- * offsets 16-byte aligned, each must hold its offset + bytes (else
- * DV_ERR_SPACE).  create allocates
+ * disjoint from each other and from the source microbatch (create returns
+ * DV_ERR_INVALID otherwise); offsets 16-byte aligned, each must hold its
+ * offset + bytes (else DV_ERR_SPACE).  create allocates
  * one stream, 64 events and the worker thread; push blocks only when 64
  * pushes are waiting for the worker.  flush blocks until everything pushed
  * has reached `dst` and returns the first error the worker met (a later

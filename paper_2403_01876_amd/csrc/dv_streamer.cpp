@@ -115,6 +115,12 @@ void release(dv_streamer* s) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+bool overlaps(const void* a, uint64_t na, const void* b, uint64_t nb) {
+  if (na == 0 || nb == 0) return false;
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
 }  // namespace
 
 extern "C" {
@@ -128,6 +134,12 @@ int dv_streamer_create(const dv_cache* src, int32_t mb, void* staging, uint64_t 
   int rc = dv_cache_bytes(src, &bytes);
   if (rc != DV_OK) return rc;
   if (mb < 0 || mb >= src->num_mb) return DV_ERR_RANGE;
+  // Staging, destination and the source microbatch must be disjoint: the
+  // worker packs into staging and copies staging to the destination.
+  if (overlaps(staging, staging_cap, src->mb_base[mb], bytes) ||
+      overlaps(dst, dst_cap, src->mb_base[mb], bytes) ||
+      overlaps(staging, staging_cap, dst, dst_cap))
+    return DV_ERR_INVALID;
   dv_streamer* s = new (std::nothrow) dv_streamer();
   if (!s) return DV_ERR_INVALID;
   s->src = *src;

@@ -249,6 +249,15 @@ def test_streamer_create_rejections():
         dv.DV_ERR_INVALID
     assert dv.lib.dv_streamer_create(dense(D=36).ref, 0, st, 1 << 20, st, 1 << 20,
                                      C.byref(h)) == dv.DV_ERR_INVALID
+    # staging, destination and the source microbatch must not overlap
+    other = FAKE + (1 << 34)
+    assert dv.lib.dv_streamer_create(c.ref, 0, st, 1 << 20, st + (1 << 19), 1 << 20,
+                                     C.byref(h)) == dv.DV_ERR_INVALID
+    assert dv.lib.dv_streamer_create(c.ref, 0, FAKE + 4096, 1 << 20, other, 1 << 20,
+                                     C.byref(h)) == dv.DV_ERR_INVALID
+    assert dv.lib.dv_streamer_create(c.ref, 0, st, 1 << 20, FAKE + 4096, 1 << 20,
+                                     C.byref(h)) == dv.DV_ERR_INVALID
+    assert h.value is None
     assert h.value is None
     for f in ("dv_streamer_flush", "dv_streamer_destroy"):
         assert getattr(dv.lib, f)(None) == dv.DV_ERR_INVALID
