@@ -129,6 +129,43 @@ def test_address_decode_brute_force(oracle_lib, seed):
         assert l0 <= l < l1 and t0[b] <= s < t1[b]
 
 
+@pytest.mark.parametrize("kind", [oracle.DENSE, oracle.PAGED, oracle.KSPLIT])
+@pytest.mark.parametrize("seed", range(6))
+def test_inverse_map_names_each_wire_source(oracle_lib, kind, seed):
+    """The inverse map the full-size GPU tests sample with, for every layout:
+    pack a cache whose every 4-byte element holds its own storage index and
+    the wire lists the sources; wire_to_storage must return the same list.
+    Sources are distinct and each lies in the (layer, sequence) ranges."""
+    r = rng(1300 + seed)
+    L, H, B = int(r.integers(1, 4)), int(r.integers(1, 5)), int(r.integers(1, 6))
+    D = int(r.choice([4, 8, 12]))  # 4-byte elements: 16-byte groups of 4
+    if kind == oracle.PAGED:
+        bs = int(r.choice([1, 3, 4]))
+        lens = [int(r.integers(0, 20)) for _ in range(B)]
+        maxb = max(1, max((n + bs - 1) // bs for n in lens)) + 1
+        bt, nb = synth.make_paged_tables(seed, lens, bs, maxb)
+        lay = oracle.Layout(oracle.PAGED, L, H, D, B, elem_bytes=4, block_size=bs,
+                            num_blocks=max(nb, 1), block_table=bt)
+        cap = lens
+    else:
+        S = int(r.integers(1, 24))
+        lay = oracle.Layout(kind, L, H, D, B, seq_cap=S, elem_bytes=4)
+        cap = [S] * B
+    t0 = np.zeros(B, np.int32)
+    t1 = np.zeros(B, np.int32)
+    for b in range(B):
+        a, e = sorted(int(v) for v in r.integers(0, cap[b] + 1, size=2))
+        t0[b], t1[b] = a, e
+    l0 = int(r.integers(0, L))
+    l1 = int(r.integers(l0, L + 1))
+    idx = np.arange(lay.storage_elems(), dtype=np.uint32)
+    wire = oracle_lib.pack(lay, idx.view(np.uint8), l0, l1, t0, t1).view(np.uint32)
+    back = oracle_lib.wire_to_storage(lay, l0, l1, t0, t1, np.arange(wire.size))
+    assert np.array_equal(back, wire.astype(np.int64))
+    assert np.unique(wire).size == wire.size
+    assert wire.size == (l1 - l0) * 2 * H * D * int((t1 - t0).sum())
+
+
 @pytest.mark.parametrize("seed", range(20))
 def test_unpack_writes_only_the_ranges(oracle_lib, seed):
     lay, buf, shp, l0, l1, t0, t1 = dense_case(100 + seed)
