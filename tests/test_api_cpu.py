@@ -261,3 +261,20 @@ def test_streamer_create_rejections():
     assert h.value is None
     for f in ("dv_streamer_flush", "dv_streamer_destroy"):
         assert getattr(dv.lib, f)(None) == dv.DV_ERR_INVALID
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """No fallback: a copy of the package without libdv.so refuses to import."""
+    import shutil
+    import subprocess
+    import sys
+    pkg = os.path.join(ROOT, "paper_2403_01876_amd")
+    dst = tmp_path / "paper_2403_01876_amd"
+    shutil.copytree(pkg, dst, ignore=shutil.ignore_patterns("*.so", "__pycache__", "csrc"))
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "try:\n    import paper_2403_01876_amd\nexcept ImportError as e:\n"
+            "    print('refused:', e); sys.exit(3)\nsys.exit(0)\n") % str(tmp_path)
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 3, r.stdout + r.stderr
+    assert "libdv.so is missing" in r.stdout
