@@ -23,7 +23,7 @@ the full-cache replica and restore (BLOOM-176B shard), and the oracle timed
 on the host cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--eager]
-                       [--extras all|calib|none] [--no-cpu-baseline]
+                       [--extras all|bulk|calib|none] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
