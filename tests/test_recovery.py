@@ -1,4 +1,6 @@
 """Controller bookkeeping of replication and recovery (CPU)."""
+import os
+
 import pytest
 
 from paper_2403_01876_amd import recovery as R
@@ -27,20 +29,44 @@ def test_resume_point_follows_the_failed_workers_replication():
     assert tab.resume_point(1) == (0, 5)  # wraps to the next step
 
 
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                      "ft_protocol_example.txt")
+
+
+def read_example(path):
+    """The worked example, converted from the paper's 1-based labels (stages,
+    microbatches, step letters A, B, C, ...) to 0-based indices."""
+    ex = {"transfers": []}
+    for line in open(path):
+        f = line.split()
+        if not f or f[0].startswith("#"):
+            continue
+        if f[0] in ("stages", "microbatches", "failed_stage"):
+            ex[f[0]] = int(f[1]) - (1 if f[0] == "failed_stage" else 0)
+        elif f[0] in ("first_unreplicated", "resume"):
+            ex[f[0]] = (int(f[1]) - 1, ord(f[2]) - ord("A"))
+        elif f[0] == "transfer":
+            ex["transfers"].append((int(f[1]) - 1, int(f[2]) - 1, f[3], int(f[4]) - 1))
+    return ex
+
+
 def test_paper_example_stage_two_fails():
-    """Four stages; stage 2 (index 1) fails after its update for microbatch 1,
-    step C had not reached stage 3: all stages resume from (1, C)."""
-    C = 2
-    tab = R.ReplicationTable(workers=4, microbatches=4)
-    for t in range(C + 1):
-        for j in range(4):
-            if R.order((j, t), 4) < R.order((1, C), 4):
-                for x in range(4):
-                    tab.report(x, j, t)
-    plan, resume = tab.recovery_plan(1)
-    assert resume == (1, C)
-    assert plan[0] == R.Transfer(sender=2, receiver=1, owner=1, into_replica=False)
-    assert plan[1] == R.Transfer(sender=0, receiver=1, owner=0, into_replica=True)
+    """The paper's worked example (fixture in tests/golden): the replication
+    status just before the failure, then the two recovery transfers and the
+    resume point the controller derives from it."""
+    ex = read_example(GOLDEN)
+    n, m, failed = ex["stages"], ex["microbatches"], ex["failed_stage"]
+    tab = R.ReplicationTable(workers=n, microbatches=m)
+    stop = R.order(ex["first_unreplicated"], m)
+    for k in range(stop):  # every (j, t) before it was replicated on every stage
+        j, t = k % m, k // m
+        for x in range(n):
+            tab.report(x, j, t)
+    plan, resume = tab.recovery_plan(failed)
+    assert resume == ex["resume"] == ex["first_unreplicated"]
+    expect = [R.Transfer(sender=snd, receiver=rcv, owner=own, into_replica=(what == "replica_of"))
+              for snd, rcv, what, own in ex["transfers"]]
+    assert plan == expect
 
 
 def test_recovery_plan_wraps_around_the_ring():
