@@ -589,14 +589,14 @@ def swap_protocol_bench(torch, dv, synth, swap_in_gbs):
     for t_ms in (0.0, 40.0, 100.0):
         lens = [w.lens.astype(np.int32).copy() for _ in range(M)]
         sw = dv.Swapper(ds, hh)
-        steps = 2 * M
-        sw.prefetch(0, lens[0])
+        sched = list(SM.swap_schedule(M, 2))
+        steps = len(sched)
+        sw.prefetch(sched[0][0], lens[sched[0][0]])
         torch.cuda.synchronize()
         marks = []
-        for k in range(steps):
-            x = k % M
-            if k + 1 < steps:
-                sw.prefetch((k + 1) % M, lens[(k + 1) % M])
+        for x, xn, _ in sched:
+            if xn is not None:
+                sw.prefetch(xn, lens[xn])
             slot = sw.begin_step(x, compute)
             c0 = torch.cuda.Event(enable_timing=True)
             c1 = torch.cuda.Event(enable_timing=True)

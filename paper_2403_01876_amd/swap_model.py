@@ -58,3 +58,23 @@ def breakeven_step_time(n_tokens: int, prompt: int, requests: int, kv_bytes_per_
         else:
             lo = mid
     return hi
+
+
+def swap_schedule(microbatches: int, rounds: int):
+    """The round-robin order of microbatch swapping (Sec. 4.2.2, Figure
+    "swapping"): microbatches are processed 0, 1, ..., M-1, 0, ... and while
+    microbatch x is processed, the next one, (x+1) % M, is swapped in and
+    the update of the previous one, (x-1) % M, is swapped out.  Yields one
+    (process, swap_in, swap_out) triple per step; swap_in is None on the last
+    step and swap_out None on the first (nothing precedes or follows them).
+    With the scheduler (dv_swapper_*) a caller issues, for each triple, the
+    prefetch of swap_in before beginning the step of `process`, and the
+    end_step of `process` after it; that end_step is the swap-out the next
+    triple lists."""
+    if microbatches < 1 or rounds < 0:
+        raise ValueError("need at least one microbatch and a non-negative round count")
+    steps = microbatches * rounds
+    for k in range(steps):
+        yield (k % microbatches,
+               (k + 1) % microbatches if k + 1 < steps else None,
+               (k - 1) % microbatches if k > 0 else None)

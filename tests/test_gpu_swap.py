@@ -11,7 +11,7 @@ torch = pytest.importorskip("torch")
 if not torch.cuda.is_available():  # pragma: no cover
     pytest.skip("no GPU", allow_module_level=True)
 
-from paper_2403_01876_amd import dv  # noqa: E402
+from paper_2403_01876_amd import dv, swap_model  # noqa: E402
 from tests import gpu_util as G  # noqa: E402
 
 
@@ -227,12 +227,12 @@ def test_swapper_round_robin(oracle_lib):
     n = dv.dv_packed_bytes(ds, 0, L, lens[0], lens[0] + 1)
     tok = torch.empty(n, dtype=torch.uint8, device=G.DEV)
     inc = torch.empty(n, dtype=torch.uint8, device=G.DEV)
-    steps = 3 * M
-    sw.prefetch(0, lens[0])
-    for k in range(steps):
-        x = k % M
-        if k + 1 < steps:
-            xn = (k + 1) % M
+    # the paper's order (swap_schedule): while x runs, prefetch x + 1; x's
+    # update leaves after its step, while x + 1 runs
+    sched = list(swap_model.swap_schedule(M, 3))
+    sw.prefetch(sched[0][0], lens[sched[0][0]])
+    for k, (x, xn, _) in enumerate(sched):
+        if xn is not None:
             sw.prefetch(xn, lens[xn])
         slot = sw.begin_step(x, compute)
         pos = lens[x]

@@ -43,3 +43,37 @@ def test_breakeven_solves_the_inequality():
     assert t <= M.transfer_time(p, R, C, bw) + 1e-15 or math.isclose(t, t_mean, rel_tol=1e-9)
     if t < M.transfer_time(p, R, C, bw):
         assert t == pytest.approx(t_mean, rel=1e-9)
+
+
+def test_swap_schedule_matches_the_papers_example():
+    """Steady state of swap_schedule against the paper's 4-stage example
+    (fixture in tests/golden, 1-based labels)."""
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                        "swap_schedule_example.txt")
+    rows, n = [], None
+    for line in open(path):
+        f = line.split()
+        if not f or f[0].startswith("#"):
+            continue
+        if f[0] == "microbatches":
+            n = int(f[1])
+        else:
+            rows.append(tuple(int(v) - 1 for v in f))
+    sched = list(M.swap_schedule(n, 3))
+    steady = sched[n:2 * n]  # the middle round: neither the first nor the last step
+    assert steady == rows
+    # edges: nothing to swap out before the first step or in after the last
+    assert sched[0] == (0, 1, None) and sched[-1] == (n - 1, None, n - 2)
+    # every microbatch is swapped in before it is processed (except the first,
+    # prefetched before the loop) and swapped out right after
+    for k, (x, nxt, prev) in enumerate(sched):
+        if k > 0:
+            assert sched[k - 1][1] == x and prev == sched[k - 1][0]
+
+
+def test_swap_schedule_single_microbatch_and_errors():
+    assert list(M.swap_schedule(1, 2)) == [(0, 0, None), (0, None, 0)]
+    assert list(M.swap_schedule(3, 0)) == []
+    with pytest.raises(ValueError):
+        list(M.swap_schedule(0, 1))
