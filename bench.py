@@ -586,7 +586,9 @@ def swap_protocol_bench(torch, dv, synth, swap_in_gbs):
     bw = swap_in_gbs * 1e9
     runs = []
     transf_ms = SM.transfer_time(int(w.lens[0]), B, kv_token, bw) * 1e3
-    for t_ms in (0.0, 40.0, 100.0):
+    # emulated steps below and above the swap-in time: the period must follow
+    # the swap-in when it is longer and the step when the step is longer
+    for t_ms in (0.0, 40.0, 100.0, 200.0):
         lens = [w.lens.astype(np.int32).copy() for _ in range(M)]
         sw = dv.Swapper(ds, hh)
         sched = list(SM.swap_schedule(M, 2))
