@@ -122,8 +122,8 @@ def test_token_increments(oracle_lib, seed):
 def paged_setup(r, seed, big_batch=False):
     L = int(r.integers(1, 4))
     H = int(r.integers(1, 12))
-    E = 2
-    D = int(r.choice([64, 128, 256]))
+    E = int(r.choice([2, 2, 1, 4]))
+    D = int(r.choice([64, 128, 256])) // E * 2  # 128, 256 or 512 bytes per token
     B = int(r.integers(65, 100)) if big_batch else int(r.integers(1, 10))
     bs = int(r.choice([1, 4, 16, 16, 32]))
     lens = [int(r.integers(0, 300)) for _ in range(B)]

@@ -62,6 +62,41 @@ def test_swap_out_in_matches_oracle(oracle_lib, seed):
     assert G.host(slot2).tobytes() == exp_slot.tobytes()
 
 
+@pytest.mark.parametrize("E", [1, 4])
+def test_swap_kernel_engine_many_sequences_other_element_sizes(oracle_lib, E):
+    """The copy-kernel engine with 100 sequences (two launch groups), 1- and
+    4-byte elements and a layer sub-range, both directions."""
+    L, H, B = 3, 2, 100
+    D = 64 if E == 4 else 128  # 256 or 128 bytes per token
+    S_dev, S_host = 40, 33
+    r = np.random.default_rng(600 + E)
+    t0 = r.integers(0, 20, size=B).astype(np.int32)
+    t1 = np.minimum(t0 + r.integers(0, 14, size=B), S_host).astype(np.int32)
+    dl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S_dev, elem_bytes=E)
+    hl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S_host, elem_bytes=E)
+    slot_h = synth.fill_bytes(dl.storage_bytes(), 31 + E)
+    slot = G.to_dev(slot_h)
+    host = pinned(hl.storage_bytes(), 0x77)
+    d = dv.Cache(dv.DV_DENSE, L, H, D, B, [slot], max_seq=S_dev, elem_bytes=E)
+    h = dv.Cache(dv.DV_DENSE, L, H, D, B, [host.data_ptr()], max_seq=S_host, elem_bytes=E,
+                 mem=dv.DV_MEM_HOST_PINNED)
+    side = torch.cuda.Stream()
+    dv.dv_swap_out(d, 0, h, 0, 1, 3, t0, t1, side)
+    side.synchronize()
+    exp_host = np.full(hl.storage_bytes(), 0x77, np.uint8)
+    oracle_lib.copy_ranges(dl, slot_h, hl, exp_host, 1, 3, t0, t1)
+    assert host.numpy().tobytes() == exp_host.tobytes()
+    host_h = synth.fill_bytes(hl.storage_bytes(), 41 + E)
+    host.copy_(torch.from_numpy(host_h))
+    slot2 = G.dev_const(dl.storage_bytes(), 0xA5)
+    d2 = dv.Cache(dv.DV_DENSE, L, H, D, B, [slot2], max_seq=S_dev, elem_bytes=E)
+    dv.dv_swap_in(h, 0, d2, 0, 1, 3, t0, t1, side)
+    side.synchronize()
+    exp_slot = np.full(dl.storage_bytes(), 0xA5, np.uint8)
+    oracle_lib.copy_ranges(hl, host_h, dl, exp_slot, 1, 3, t0, t1)
+    assert G.host(slot2).tobytes() == exp_slot.tobytes()
+
+
 @pytest.mark.parametrize("case", ["delta-uniform", "delta-ragged", "wide-uniform",
                                   "wide-ragged", "mixed"])
 def test_swap_engines_match_oracle(oracle_lib, case):
