@@ -278,3 +278,50 @@ def test_binding_fails_loudly_without_the_library(tmp_path):
                        timeout=300)
     assert r.returncode == 3, r.stdout + r.stderr
     assert "libdv.so is missing" in r.stdout
+
+
+C_PROGRAM = r"""
+#include <stdio.h>
+#include <string.h>
+#include "dv.h"
+
+int main(void) {
+  void* bases[1] = {(void*)(unsigned long long)(1ull << 40)};
+  dv_cache c;
+  memset(&c, 0, sizeof c);
+  c.kind = DV_DENSE; c.mem = DV_MEM_DEVICE; c.elem_bytes = 2;
+  c.num_layers = 10; c.num_heads = 40; c.head_dim = 128; c.batch = 8; c.max_seq = 2048;
+  c.num_mb = 1; c.mb_base = bases;
+  int32_t t1[8] = {512, 600, 700, 800, 900, 1000, 1024, 0};
+  uint64_t bytes = 0, cache = 0;
+  if (dv_packed_bytes(&c, 0, 10, NULL, t1, &bytes) != DV_OK) return 1;
+  if (dv_cache_bytes(&c, &cache) != DV_OK) return 2;
+  /* validation errors come back before anything reaches the runtime */
+  int rc = dv_stream_out_prompt(&c, -1, 0, 10, NULL, t1, NULL, 0, NULL, NULL);
+  printf("%llu %llu %d %s %d\n", (unsigned long long)bytes, (unsigned long long)cache, rc,
+         dv_status_string(rc), dv_api_version());
+  return 0;
+}
+"""
+
+
+def test_header_and_library_from_c(tmp_path):
+    """The boundary from plain C: include/dv.h compiles as C99 with warnings
+    as errors, and a program linked against libdv.so sizes a stream and gets
+    validation errors back (no GPU needed)."""
+    import subprocess
+    src = tmp_path / "use_dv.c"
+    src.write_text(C_PROGRAM)
+    exe = tmp_path / "use_dv"
+    libdir = os.path.dirname(dv.LIB_PATH)
+    cc = subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic",
+                         "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe),
+                         "-L", libdir, "-ldv", "-Wl,-rpath," + libdir],
+                        capture_output=True, text=True, timeout=120)
+    assert cc.returncode == 0, cc.stderr
+    run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert run.returncode == 0, run.stdout + run.stderr
+    n, cache, rc, *rest = run.stdout.split()
+    assert int(n) == 10 * 2 * 40 * 128 * 2 * (512 + 600 + 700 + 800 + 900 + 1000 + 1024)
+    assert int(cache) == 10 * 2 * 8 * 40 * 2048 * 128 * 2
+    assert int(rc) == dv.DV_ERR_RANGE and rest[-1] == "1"
