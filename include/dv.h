@@ -229,13 +229,15 @@ DV_API int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev
  * GPU_MAX_HW_QUEUES hardware queues (4 by default) and streams sharing a
  * queue execute in order, so a process with many streams should raise it
  * (measured on MI355X: with 4 queues and torch's stream pool the swap-in
- * and the step serialised; with 8 the swap-in hid behind the step).  Both caches DV_DENSE with equal
- * shapes (capacities may differ), dev in DV_MEM_DEVICE, host in
- * DV_MEM_HOST_PINNED.  One scheduler per host thread.
+ * and the step serialised; with 8 the swap-in hid behind the step).  Both
+ * caches DV_DENSE with equal shapes (capacities may differ), dev in
+ * DV_MEM_DEVICE, host in DV_MEM_HOST_PINNED.  One scheduler per host thread.
+ * prefetch and end_step check their ranges against both the slots and the
+ * host mirrors before enqueuing anything; a refused call changes nothing.
  * Errors: DV_ERR_INVALID (bad arguments; prefetch into a slot whose
  * occupant's step has not ended), DV_ERR_RANGE (microbatch outside `host`;
- * begin/end of a microbatch not prefetched), DV_ERR_UNSUPPORTED, DV_ERR_HIP,
- * plus those of dv_swap_in / dv_swap_out. */
+ * begin/end of a microbatch not prefetched; ranges that do not fit),
+ * DV_ERR_UNSUPPORTED, DV_ERR_HIP. */
 typedef struct dv_swapper dv_swapper;
 DV_API int dv_swapper_create(const dv_cache* dev_slots, const dv_cache* host, dv_swapper** out);
 DV_API int dv_swapper_prefetch(dv_swapper* s, int32_t mb, const int32_t* len);
