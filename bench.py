@@ -952,6 +952,7 @@ def cpu_baseline():
     c = time.perf_counter()
     assert rc == 0
     secs = c - a
+    del cache, recv, wire
     return {
         "value": round(2 * 2 * n / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
         "sample": (f"prompt stream-out + stream-in of the OPT-13B stage, all {w.layers} "
@@ -959,7 +960,76 @@ def cpu_baseline():
                    f"({b - a:.2f} s out, {c - b:.2f} s in)"),
         "host_cpu": cpu_model(),
         "affinity_cores": len(os.sched_getaffinity(0)),
+        "per_op": cpu_baseline_per_op(orc),
     }
+
+
+def cpu_baseline_per_op(orc):
+    """The oracle on the other operations the benchmark times, each on a
+    bounded sample of its workload (layer 0 of the stage, or one decode
+    step), in the same 2 x payload GB/s."""
+    import oracle
+    import synth
+
+    out = {}
+
+    def rate(nbytes, fn):
+        a = time.perf_counter()
+        fn()
+        return round(2 * nbytes / (time.perf_counter() - a) / 1e9, 3)
+
+    # paged gather / scatter: LLaMA-2-70B pool, layer 0 of 20
+    w = synth.make_workload(4)
+    la = oracle.Layout(oracle.PAGED, 1, w.heads, w.head_dim, w.batch, block_size=w.block_size,
+                       num_blocks=w.num_blocks, block_table=w.block_table_a)
+    lb = oracle.Layout(oracle.PAGED, 1, w.heads, w.head_dim, w.batch, block_size=w.block_size,
+                       num_blocks=w.num_blocks, block_table=w.block_table_b)
+    pool = synth.fill_bytes(la.storage_bytes(), w.data_seed)
+    t0, t1 = w.prompt_ranges()
+    box = {}
+    g = rate(orc.wire_elems(la, 0, 1, t0, t1) * 2,
+             lambda: box.setdefault("wire", orc.pack(la, pool, 0, 1, t0, t1)))
+    recv = np.zeros(lb.storage_bytes(), np.uint8)
+    sc = rate(box["wire"].nbytes, lambda: orc.unpack(lb, recv, 0, 1, t0, t1, box["wire"]))
+    out["llama2-70b-paged"] = {"gather_GBps_2x": g, "scatter_GBps_2x": sc,
+                               "sample": f"layer 0 of {w.layers}, {box['wire'].nbytes} B payload"}
+    del pool, recv, box
+    # split key: OPT-13B stage, layer 0 of 10
+    w = synth.make_workload(1)
+    lk = oracle.Layout(oracle.KSPLIT, 1, w.heads, w.head_dim, w.batch, seq_cap=w.max_seq)
+    cache = synth.fill_bytes(lk.storage_bytes(), w.data_seed)
+    t0, t1 = w.prompt_ranges()
+    box = {}
+    pk = rate(orc.wire_elems(lk, 0, 1, t0, t1) * 2,
+              lambda: box.setdefault("wire", orc.pack(lk, cache, 0, 1, t0, t1)))
+    recv = np.zeros_like(cache)
+    uk = rate(box["wire"].nbytes, lambda: orc.unpack(lk, recv, 0, 1, t0, t1, box["wire"]))
+    out["opt13b-stage split-key"] = {"pack_GBps_2x": pk, "unpack_GBps_2x": uk,
+                                     "sample": f"layer 0 of {w.layers}, {box['wire'].nbytes} B "
+                                               "payload"}
+    # one decode-step increment of the OPT-13B stage, layer 0 (the split-key
+    # sample's value half is dense, so its cache serves as a dense layer)
+    ld = oracle.Layout(oracle.DENSE, 1, w.heads, w.head_dim, w.batch, seq_cap=w.max_seq)
+    p = w.step_positions(0)
+    inc = orc.wire_elems(ld, 0, 1, p, p + 1) * 2
+    box = {}
+    ti = rate(inc, lambda: [box.setdefault(k, orc.pack(ld, cache, 0, 1, p, p + 1))
+                            for k in range(10)])
+    out["opt13b-stage increment"] = {"pack_GBps_2x": round(ti * 10, 3),
+                                     "sample": f"one step of layer 0, {inc} B, 10 calls"}
+    del cache, recv, box
+    # swap copy: OPT-66B microbatch, layer 0 of 16, slot to a 1024-token mirror
+    w = synth.make_workload(2)
+    sd = oracle.Layout(oracle.DENSE, 1, w.heads, w.head_dim, w.batch, seq_cap=w.max_seq)
+    hd = oracle.Layout(oracle.DENSE, 1, w.heads, w.head_dim, w.batch, seq_cap=1024)
+    slot = synth.fill_bytes(sd.storage_bytes(), w.data_seed)
+    host = np.zeros(hd.storage_bytes(), np.uint8)
+    t0, t1 = w.prompt_ranges()
+    moved = orc.wire_elems(sd, 0, 1, t0, t1) * 2
+    sw = rate(moved, lambda: orc.copy_ranges(sd, slot, hd, host, 0, 1, t0, t1))
+    out["opt66b-stage swap copy"] = {"GBps_2x": sw, "sample": f"layer 0 of {w.layers}, "
+                                                              f"{moved} B"}
+    return out
 
 
 def counted_traffic():
