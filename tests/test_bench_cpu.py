@@ -1,0 +1,40 @@
+"""bench.py's host-side contract without a GPU: it refuses more than one
+GPU with a message, and the counted-traffic figure is read only while the
+kernel sources hash to the value the committed counter summary records."""
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2
+    assert "one GPU only" in r.stderr and r.stdout == ""
+
+
+def test_counted_traffic_follows_the_kernel_sources(tmp_path, monkeypatch):
+    t = bench.counted_traffic()
+    assert t is None or 2 * 1282252800 <= t <= 1.01 * 2 * 1282252800
+    # a summary whose recorded hash does not match the sources gives None
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    src = open(os.path.join(ROOT, "profiles", "dense_runs_hbm_traffic_opt13b_stage.md")).read()
+    lines = [("kernel_source_sha256: " + "0" * 64) if ln.startswith("kernel_source_sha256:")
+             else ln for ln in src.splitlines()]
+    (prof / "dense_runs_hbm_traffic_opt13b_stage.md").write_text("\n".join(lines) + "\n")
+    csrc = tmp_path / "paper_2403_01876_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    for f in ("dv_kernels.hip", "dv_internal.h"):
+        (csrc / f).write_bytes(open(os.path.join(ROOT, "paper_2403_01876_amd", "csrc", f),
+                                    "rb").read())
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.counted_traffic() is None
+    # and a missing summary gives None too
+    (prof / "dense_runs_hbm_traffic_opt13b_stage.md").unlink()
+    assert bench.counted_traffic() is None
