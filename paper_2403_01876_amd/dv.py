@@ -118,8 +118,14 @@ def _addr(x) -> int:
 
 
 def _stream(s) -> int:
+    """A hipStream_t: an int passes through, a torch stream gives its handle,
+    None means torch's current stream (as for torch's own operations)."""
     if s is None:
-        return 0
+        import torch
+        try:
+            return torch.cuda.current_stream().cuda_stream
+        except RuntimeError:  # no device: the null stream (the runtime reports the rest)
+            return 0
     if isinstance(s, int):
         return s
     return s.cuda_stream

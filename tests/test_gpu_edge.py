@@ -339,3 +339,27 @@ def test_per_region_baseline_matches_buffered(oracle_lib, seed):
     torch.cuda.synchronize()
     assert G.host(d_buf)[:n].tobytes() == exp.tobytes()
     assert h_buf.numpy()[:n].tobytes() == exp.tobytes()
+
+
+def test_binding_follows_torchs_current_stream(oracle_lib):
+    """stream=None means torch's current stream: under torch.cuda.stream(s)
+    the pack runs after the work already queued on s (here a long spin and
+    then the fill of its source), never on a stream unordered with it."""
+    L, H, D, B, S = 2, 4, 128, 3, 64
+    lay = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S)
+    host = synth.fill_bytes(lay.storage_bytes(), 91)
+    cache = G.dev_const(lay.storage_bytes(), 0)
+    staged = G.to_dev(host)
+    c = dv.Cache(dv.DV_DENSE, L, H, D, B, [cache], max_seq=S)
+    t0 = np.zeros(B, np.int32)
+    t1 = np.array([64, 10, 33], np.int32)
+    n = dv.dv_packed_bytes(c, 0, L, t0, t1)
+    wire = G.dev_const(n, 0)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        torch.cuda._sleep(50_000_000)  # tens of ms on the side stream
+        cache.copy_(staged)
+        dv.dv_stream_out_prompt(c, 0, 0, L, t0, t1, wire, n)  # stream=None
+    torch.cuda.synchronize()
+    assert G.host(wire).tobytes() == oracle_lib.pack(lay, host, 0, L, t0, t1).tobytes()
