@@ -86,6 +86,58 @@ def test_token_streaming_many_steps(oracle_lib):
         assert h[i * inc:(i + 1) * inc].tobytes() == tok_wires[i].tobytes(), i
 
 
+def test_paged_source_layer_by_layer_and_from_two_threads(oracle_lib):
+    """A paged source cache (random block table) streamed layer by layer into
+    device memory, the layers pushed from two host threads at once (each
+    layer to its own offset), then each sequence's next token; every byte
+    equals the oracle's pack."""
+    import threading
+    L, H, D, B, bs = 6, 4, 128, 5, 16
+    lens = [70, 3, 0, 48, 129]
+    maxb = max((n + 1 + bs - 1) // bs for n in lens) + 1
+    bt, nb = synth.make_paged_tables(61, [n + 1 for n in lens], bs, maxb)
+    lay = oracle.Layout(oracle.PAGED, L, H, D, B, block_size=bs, num_blocks=nb, block_table=bt)
+    host_pool = synth.fill_bytes(lay.storage_bytes(), 62)
+    pool = G.to_dev(host_pool)
+    btd = G.to_dev(bt)
+    c = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool], block_size=bs, num_blocks=nb,
+                 max_blocks=maxb, block_tables=[btd])
+    zero = np.zeros(B, np.int32)
+    t1 = np.array(lens, np.int32)
+    per_layer = [dv.dv_packed_bytes(c, l, l + 1, zero, t1) for l in range(L)]
+    offs = np.concatenate([[0], np.cumsum(per_layer)]).astype(np.int64)
+    inc = dv.dv_packed_bytes(c, 0, L, t1, t1 + 1)
+    total = int(offs[-1]) + inc
+    staging = G.dev_const(total, 0)
+    dst = G.dev_const(total, 0x11)
+    s = dv.Streamer(c, 0, staging, total, dst, total)
+    errors = []
+
+    def push_layers(layers):
+        try:
+            for l in layers:
+                s.push(l, l + 1, zero, t1, int(offs[l]))
+        except Exception as e:  # surfaced below
+            errors.append(e)
+
+    threads = [threading.Thread(target=push_layers, args=(range(k, L, 2),)) for k in (0, 1)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    assert s.push(0, L, t1, t1 + 1, int(offs[-1])) == inc
+    assert s.flush() == dv.DV_OK
+    s.close()
+    torch.cuda.synchronize()
+    got = G.host(dst)
+    for l in range(L):
+        exp = oracle_lib.pack(lay, host_pool, l, l + 1, zero, t1)
+        assert got[offs[l]:offs[l + 1]].tobytes() == exp.tobytes(), l
+    exp = oracle_lib.pack(lay, host_pool, 0, L, t1, t1 + 1)
+    assert got[offs[-1]:].tobytes() == exp.tobytes()
+
+
 def test_streamer_errors_surface():
     L, H, D, B, S = 1, 1, 64, 2, 16
     cache = G.dev_const(L * 2 * B * H * S * D * 2, 0)
