@@ -48,7 +48,8 @@
 extern "C" {
 #endif
 
-#define DV_API_VERSION 1
+/* 2: dv_cache gained block_owner (the optional owner-map workspace). */
+#define DV_API_VERSION 2
 
 /* The library is built with hidden visibility; only these calls export. */
 #define DV_API __attribute__((visibility("default")))

@@ -50,6 +50,9 @@ class dv_cache(ctypes.Structure):
     ]
 
 
+API_VERSION = 2  # DV_API_VERSION the dv_cache layout above matches
+
+
 def _load():
     # torch's libraries need the HIP runtime by file name (libamdhip64.so)
     # while libdv.so needs it by SONAME (libamdhip64.so.7): importing torch
@@ -88,6 +91,9 @@ def _load():
         f.restype = ctypes.c_int
     lib.dv_status_string.argtypes = [ctypes.c_int]
     lib.dv_status_string.restype = ctypes.c_char_p
+    if lib.dv_api_version() != API_VERSION:
+        raise ImportError(f"{LIB_PATH} is API version {lib.dv_api_version()}, this binding "
+                          f"expects {API_VERSION}: rebuild with __graft_entry__.build()")
     return lib
 
 

@@ -26,7 +26,7 @@ def test_library_exports_every_declared_function():
     lib = ctypes.CDLL(dv.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
-    assert dv.dv_api_version() == 1
+    assert dv.dv_api_version() == dv.API_VERSION == 2
 
 
 def test_status_strings():
@@ -324,4 +324,4 @@ def test_header_and_library_from_c(tmp_path):
     n, cache, rc, *rest = run.stdout.split()
     assert int(n) == 10 * 2 * 40 * 128 * 2 * (512 + 600 + 700 + 800 + 900 + 1000 + 1024)
     assert int(cache) == 10 * 2 * 8 * 40 * 2048 * 128 * 2
-    assert int(rc) == dv.DV_ERR_RANGE and rest[-1] == "1"
+    assert int(rc) == dv.DV_ERR_RANGE and rest[-1] == "2"
