@@ -183,6 +183,19 @@ DV_API int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int3
 DV_API int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
                  const int32_t* t1, const void* src, uint64_t src_bytes, void* stream);
 
+/* Debug check of a paged table over token ranges [t0[b], t1[b]) (t0 may be
+ * NULL): writes to `counts` (device int32 [num_blocks], caller owned,
+ * 4-byte aligned, disjoint from the pool) how many (sequence, logical
+ * block) entries that hold a streamed token map to each pool block.  A
+ * count above 1 marks a block that dv_stream_in would write twice, which
+ * the paged receivers' precondition rules out; entries outside
+ * [0, num_blocks) are not counted.  Enqueued on `stream` (two small
+ * launches); read `counts` after synchronising it.
+ * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_UNSUPPORTED (not DV_PAGED),
+ * DV_ERR_HIP. */
+DV_API int dv_block_claims(const dv_cache* c, int32_t mb, const int32_t* t0, const int32_t* t1,
+                           int32_t* counts, void* stream);
+
 /* Microbatch swap-out: copy layers [l0, l1), tokens [t0[b], t1[b]) of device
  * slot `slot` of `dev` to host microbatch `host_mb` of `host`, at equal
  * logical coordinates; all other host bytes are left as they were.  Both

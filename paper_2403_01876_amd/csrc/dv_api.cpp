@@ -514,6 +514,40 @@ int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const 
                     static_cast<hipStream_t>(stream));
 }
 
+int dv_block_claims(const dv_cache* c, int32_t mb, const int32_t* t0, const int32_t* t1,
+                    int32_t* counts, void* stream) {
+  View v;
+  int rc = view_of(c, mb, &v);
+  if (rc != DV_OK) return rc;
+  if (v.kind != DV_PAGED) return DV_ERR_UNSUPPORTED;
+  std::vector<int32_t> r0, rn;
+  int64_t N = 0;
+  rc = ranges_of(v, 0, (int32_t)v.L, t0, t1, &r0, &rn, &N);
+  if (rc != DV_OK) return rc;
+  if (!counts || (reinterpret_cast<uintptr_t>(counts) & 3u) != 0) return DV_ERR_INVALID;
+  if (overlaps(counts, (uint64_t)v.NB * 4, v.base, v.bytes)) return DV_ERR_INVALID;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  for (int64_t g0 = 0; g0 < v.B; g0 += kSeqPerLaunch) {
+    const int nseq = (int)std::min<int64_t>(kSeqPerLaunch, v.B - g0);
+    dv::OwnerArgs o;
+    memset(&o, 0, sizeof o);
+    o.owner = counts;
+    o.bt = v.bt;
+    o.nseq = nseq;
+    o.block_size = (int32_t)v.bs;
+    o.num_blocks = (int32_t)v.NB;
+    o.max_blocks = (int32_t)v.max_blocks;
+    o.b0 = (int32_t)g0;
+    for (int i = 0; i < nseq; ++i) {
+      o.r.t0[i] = r0[g0 + i];
+      o.r.n[i] = rn[g0 + i];
+    }
+    const hipError_t e = dv::launch_block_claims(o, g0 == 0, st);
+    if (e != hipSuccess) return hip_fail(e, "block claims launch");
+  }
+  return DV_OK;
+}
+
 int dv_swap_out(const dv_cache* dev, int32_t slot, const dv_cache* host, int32_t host_mb,
                 int32_t l0, int32_t l1, const int32_t* t0, const int32_t* t1, void* stream) {
   return swap_copy(dev, slot, host, host_mb, l0, l1, t0, t1, stream, DV_MEM_DEVICE,

@@ -70,6 +70,7 @@ struct OwnerArgs {
   int32_t* owner;
   const int32_t* bt;
   int32_t nseq, block_size, num_blocks, max_blocks;
+  int32_t b0, pad;  // block claims: index of the launch's first sequence
   SeqRanges r;
 };
 
@@ -129,6 +130,10 @@ hipError_t launch_paged(int dir, const PagedArgs& a, uint32_t tiles_per_slab, ui
                         hipStream_t s);
 // Clears the owner map and fills it from the table (two launches).
 hipError_t launch_owner_map(const OwnerArgs& a, hipStream_t s);
+// Counts, per pool block, the table entries over the ranges of sequences
+// [b0, b0 + nseq) that map to it, into `a.owner` (int32 counts), clearing
+// the counts first when `clear` is set.
+hipError_t launch_block_claims(const OwnerArgs& a, bool clear, hipStream_t s);
 hipError_t launch_token(int dir, const TokenArgs& a, uint32_t units_per_slab, uint32_t nslabs,
                         hipStream_t s);
 hipError_t launch_ksplit(int dir, const KsplitArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,

@@ -210,6 +210,23 @@ __global__ void __launch_bounds__(kThreads) owner_clear_kernel(OwnerArgs a) {
   if (i < a.num_blocks) a.owner[i] = -1;
 }
 
+__global__ void __launch_bounds__(kThreads) claims_clear_kernel(OwnerArgs a) {
+  const int i = blockIdx.x * kThreads + threadIdx.x;
+  if (i < a.num_blocks) a.owner[i] = 0;
+}
+
+// One lane per table entry, as owner_build_kernel; counts instead of storing.
+__global__ void __launch_bounds__(kThreads) claims_count_kernel(OwnerArgs a) {
+  const int b = blockIdx.y;
+  const int j = blockIdx.x * kThreads + threadIdx.x;
+  if (j >= a.max_blocks) return;
+  const int t0 = a.r.t0[b], t1 = t0 + a.r.n[b];
+  if (t0 >= t1 || (j + 1) * a.block_size <= t0 || j * a.block_size >= t1) return;
+  const int blk = a.bt[(int64_t)(a.b0 + b) * a.max_blocks + j];
+  if (blk < 0 || blk >= a.num_blocks) return;
+  atomicAdd(&a.owner[blk], 1);
+}
+
 __global__ void __launch_bounds__(kThreads) owner_build_kernel(OwnerArgs a) {
   const int b = blockIdx.y;
   const int j = blockIdx.x * kThreads + threadIdx.x;
@@ -452,6 +469,16 @@ hipError_t launch_owner_map(const OwnerArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   const uint32_t cols = (uint32_t)((a.max_blocks + kThreads - 1) / kThreads);
   return launch((const void*)&owner_build_kernel, dim3(cols, a.nseq), a, s);
+}
+
+hipError_t launch_block_claims(const OwnerArgs& a, bool clear, hipStream_t s) {
+  if (clear) {
+    const uint32_t n = (uint32_t)((a.num_blocks + kThreads - 1) / kThreads);
+    const hipError_t e = launch((const void*)&claims_clear_kernel, dim3(n), a, s);
+    if (e != hipSuccess) return e;
+  }
+  const uint32_t cols = (uint32_t)((a.max_blocks + kThreads - 1) / kThreads);
+  return launch((const void*)&claims_count_kernel, dim3(cols, a.nseq), a, s);
 }
 
 hipError_t launch_token(int dir, const TokenArgs& a, uint32_t units_per_slab, uint32_t nslabs,

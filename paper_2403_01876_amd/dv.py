@@ -73,6 +73,7 @@ def _load():
         "dv_stream_in": [P, i32, i32, i32, vp, vp, vp, u64, vp],
         "dv_swap_out": [P, i32, P, i32, i32, i32, vp, vp, vp],
         "dv_swap_in": [P, i32, P, i32, i32, i32, vp, vp, vp],
+        "dv_block_claims": [P, i32, vp, vp, vp, vp],
         "dv_api_version": [],
         "dv_swapper_create": [P, P, ctypes.POINTER(vp)],
         "dv_swapper_prefetch": [vp, i32, vp],
@@ -104,7 +105,8 @@ EXPORTS = ("dv_cache_bytes", "dv_packed_bytes", "dv_stream_out_prompt", "dv_stre
            "dv_stream_in", "dv_swap_out", "dv_swap_in", "dv_status_string", "dv_api_version",
            "dv_swapper_create", "dv_swapper_prefetch", "dv_swapper_begin_step",
            "dv_swapper_end_step", "dv_swapper_sync", "dv_swapper_destroy",
-           "dv_streamer_create", "dv_streamer_push", "dv_streamer_flush", "dv_streamer_destroy")
+           "dv_streamer_create", "dv_streamer_push", "dv_streamer_flush", "dv_streamer_destroy",
+           "dv_block_claims")
 
 
 def status_string(status: int) -> str:
@@ -223,6 +225,16 @@ def dv_stream_in(dst: Cache, mb: int, l0: int, l1: int, t0, t1, src, src_bytes: 
     a1, p1 = _i32(t1)
     rc = lib.dv_stream_in(dst.ref, mb, l0, l1, p0, p1, _addr(src), src_bytes, _stream(stream))
     return _check(rc, "dv_stream_in", check)
+
+
+def dv_block_claims(cache: Cache, mb: int, t0, t1, counts, stream=None,
+                    check: bool = True) -> int:
+    """Per-block claim counts of a paged table over the ranges, into the
+    device int32 buffer `counts` (read it after synchronising)."""
+    a0, p0 = _i32(t0)
+    a1, p1 = _i32(t1)
+    rc = lib.dv_block_claims(cache.ref, mb, p0, p1, _addr(counts), _stream(stream))
+    return _check(rc, "dv_block_claims", check)
 
 
 def dv_swap_out(dev: Cache, slot: int, host: Cache, host_mb: int, l0: int, l1: int, t0, t1,

@@ -97,6 +97,23 @@ def test_negative_microbatch_and_slot_are_rejected():
     assert dv.dv_cache_bytes(c) == 2 * 2 * 4 * 3 * 50 * 64 * 2
 
 
+def test_block_claims_rejections():
+    d = dense()
+    z = np.zeros(4, np.int32)
+    t1 = np.full(4, 10, np.int32)
+    cnt = FAKE + (1 << 36)
+    assert dv.dv_block_claims(d, 0, z, t1, cnt, check=False) == dv.DV_ERR_UNSUPPORTED
+    p = dv.Cache(dv.DV_PAGED, 2, 3, 64, 4, [FAKE], block_size=16, num_blocks=8, max_blocks=4,
+                 block_tables=[FAKE + (1 << 35)])
+    assert dv.dv_block_claims(p, 1, z, t1, cnt, check=False) == dv.DV_ERR_RANGE
+    assert dv.dv_block_claims(p, -1, z, t1, cnt, check=False) == dv.DV_ERR_RANGE
+    assert dv.dv_block_claims(p, 0, z, np.full(4, 65, np.int32), cnt,
+                              check=False) == dv.DV_ERR_RANGE
+    assert dv.dv_block_claims(p, 0, z, t1, None, check=False) == dv.DV_ERR_INVALID
+    assert dv.dv_block_claims(p, 0, z, t1, cnt + 2, check=False) == dv.DV_ERR_INVALID
+    assert dv.dv_block_claims(p, 0, z, t1, FAKE + 64, check=False) == dv.DV_ERR_INVALID
+
+
 def test_owner_workspace_rejections():
     """A paged receiver's owner-map workspace must be 4-byte aligned and must
     not overlap the pool or the source buffer; all checked on the host."""

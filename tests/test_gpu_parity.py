@@ -229,6 +229,45 @@ def test_paged_scatter_pool_order(oracle_lib, seed):
             assert (w[: nb * 4] == 0x7E).all()
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_block_claims_count_table_entries(seed):
+    """dv_block_claims against a plain count of the table entries over the
+    ranges, with duplicated and unmapped entries planted in the table, and
+    more than 64 sequences for some seeds."""
+    r = np.random.default_rng(1500 + seed)
+    L, H, D, B, E, bs, lens, maxb, bt, nb = paged_setup(r, seed, big_batch=(seed % 3 == 2))
+    bt = bt.copy()
+    valid = np.argwhere(bt >= 0)
+    for _ in range(3):  # duplicates
+        if len(valid) >= 2:
+            a, b = valid[r.integers(0, len(valid), size=2)]
+            bt[a[0], a[1]] = bt[b[0], b[1]]
+    if len(valid):
+        k = valid[r.integers(0, len(valid))]
+        bt[k[0], k[1]] = nb + 5  # unmapped: outside the pool
+    t0 = np.zeros(B, np.int32)
+    t1 = np.zeros(B, np.int32)
+    for b in range(B):
+        a, c = sorted(int(v) for v in r.integers(0, lens[b] + 1, size=2))
+        t0[b], t1[b] = a, c
+    exp = np.zeros(nb, np.int64)
+    for b in range(B):
+        if t1[b] > t0[b]:
+            for j in range(t0[b] // bs, (t1[b] - 1) // bs + 1):
+                if 0 <= bt[b, j] < nb:
+                    exp[bt[b, j]] += 1
+    pool = G.dev_const(L * 2 * nb * H * bs * D * E, 0)
+    btd = G.to_dev(bt)
+    c = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool], elem_bytes=E, block_size=bs, num_blocks=nb,
+                 max_blocks=maxb, block_tables=[btd])
+    counts = G.dev_const(nb * 4 + 64, 0x7E)
+    dv.dv_block_claims(c, 0, t0, t1, counts, stream())
+    torch.cuda.synchronize()
+    got = G.host(counts)
+    assert (got[nb * 4:] == 0x7E).all(), "wrote past the counts"
+    assert np.array_equal(got[: nb * 4].view(np.int32), exp.astype(np.int32))
+
+
 @pytest.mark.parametrize("seed", range(8))
 def test_paged_token_increments(oracle_lib, seed):
     r = np.random.default_rng(300 + seed)
