@@ -150,6 +150,10 @@ class Cache:
         """``block_owners``: optional per-microbatch int32 [num_blocks] device
         workspaces (None entries allowed) that let bulk paged stream-ins
         scatter in pool order."""
+        # Tensors and arrays given here stay referenced for the descriptor's
+        # life, so a temporary cannot be freed while its address is in use.
+        self._keep = [x for x in list(bases) + list(block_tables or []) +
+                      list(block_owners or []) if not isinstance(x, int) and x is not None]
         self.bases = (ctypes.c_void_p * len(bases))(*[_addr(b) for b in bases])
         self.tables = self.owners = None
         if block_tables is not None:

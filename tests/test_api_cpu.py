@@ -342,3 +342,27 @@ def test_header_and_library_from_c(tmp_path):
     assert int(n) == 10 * 2 * 40 * 128 * 2 * (512 + 600 + 700 + 800 + 900 + 1000 + 1024)
     assert int(cache) == 10 * 2 * 8 * 40 * 2048 * 128 * 2
     assert int(rc) == dv.DV_ERR_RANGE and rest[-1] == "2"
+
+
+def test_descriptor_keeps_its_buffers_alive():
+    """A descriptor built from temporaries keeps them referenced, so their
+    memory cannot be reused while the descriptor holds their addresses."""
+    import gc
+    import weakref
+
+    class Buf:
+        def __init__(self):
+            self.a = np.zeros(64, np.uint8)
+
+        def data_ptr(self):
+            return self.a.ctypes.data
+
+    b = Buf()
+    ref = weakref.ref(b)
+    c = dv.Cache(dv.DV_DENSE, 1, 1, 16, 1, [b], max_seq=1)
+    del b
+    gc.collect()
+    assert ref() is not None
+    del c
+    gc.collect()
+    assert ref() is None
