@@ -307,10 +307,12 @@ def dv_swapper_create(dev_slots: Cache, host: Cache) -> Swapper:
 
 
 class Streamer:
-    """The background streamer (dv_streamer_*); keeps its descriptor."""
+    """The background streamer (dv_streamer_*); keeps its descriptor and its
+    staging and destination buffers alive while it exists."""
 
     def __init__(self, src: Cache, mb: int, staging, staging_cap: int, dst, dst_cap: int):
         self.src = src
+        self._keep = [x for x in (staging, dst) if not isinstance(x, int)]
         h = ctypes.c_void_p(0)
         _check(lib.dv_streamer_create(src.ref, mb, _addr(staging), staging_cap, _addr(dst),
                                       dst_cap, ctypes.byref(h)), "dv_streamer_create", True)
