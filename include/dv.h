@@ -62,7 +62,13 @@ typedef enum {
   DV_ERR_RANGE = -2,       /* microbatch/slot index, layer range or token range outside the
                               descriptor */
   DV_ERR_SPACE = -3,       /* destination capacity (or source size) below the stream size */
-  DV_ERR_UNSUPPORTED = -4, /* well-formed but not handled (swap of a paged or split-key cache) */
+  DV_ERR_UNSUPPORTED = -4, /* well-formed but not handled: swap of a paged or split-key cache;
+                              a split-key cache with more than 32 16-byte groups per token;
+                              extents past the kernels' 32-bit index arithmetic -- token
+                              capacity (max_seq, or max_blocks*block_size) above 2^24,
+                              head_dim*elem_bytes above 2^20 bytes, num_heads*head_dim*
+                              elem_bytes above 2^24 bytes, capacity*head_dim*elem_bytes above
+                              2^34 bytes, or a launch of 2^31 or more workgroups */
   DV_ERR_HIP = -5          /* the HIP runtime refused to enqueue the work */
 } dv_status;
 

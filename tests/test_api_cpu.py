@@ -366,3 +366,31 @@ def test_descriptor_keeps_its_buffers_alive():
     del c
     gc.collect()
     assert ref() is None
+
+
+def test_extent_limits_at_and_past_the_boundary():
+    """Each extent limit the header lists: the largest accepted value sizes
+    its stream, one step past it is DV_ERR_UNSUPPORTED (sizing calls only)."""
+    z1 = np.zeros(1, np.int32)
+    U = dv.DV_ERR_UNSUPPORTED
+
+    def sized(c, t1):
+        return dv.dv_packed_bytes(c, 0, 1, z1, np.array([t1], np.int32), check=False)
+
+    # token capacity 2^24 (dense max_seq)
+    assert sized(dense(L=1, H=1, D=8, B=1, S=1 << 24), 1 << 24) == (0, 2 * 16 << 24)
+    assert sized(dense(L=1, H=1, D=8, B=1, S=(1 << 24) + 1), 1)[0] == U
+    # token capacity of a paged table: max_blocks * block_size
+    paged = lambda maxb: dv.Cache(dv.DV_PAGED, 1, 1, 8, 1, [FAKE], block_size=16,  # noqa: E731
+                                  num_blocks=4, max_blocks=maxb, block_tables=[FAKE])
+    assert sized(paged(1 << 20), 1 << 24) == (0, 2 * 16 << 24)
+    assert sized(paged((1 << 20) + 1), 1)[0] == U
+    # head_dim * elem_bytes = 2^20 bytes (2^16 units)
+    assert sized(dense(L=1, H=1, D=1 << 19, B=1, S=2), 1) == (0, 2 << 20)
+    assert sized(dense(L=1, H=1, D=(1 << 19) + 8, B=1, S=2), 1)[0] == U
+    # heads * head_dim * elem_bytes = 2^24 bytes
+    assert sized(dense(L=1, H=1 << 16, D=128, B=1, S=2), 1) == (0, 2 << 24)
+    assert sized(dense(L=1, H=(1 << 16) + 1, D=128, B=1, S=2), 1)[0] == U
+    # capacity * head_dim * elem_bytes = 2^34 bytes
+    assert sized(dense(L=1, H=1, D=512, B=1, S=1 << 24), 1) == (0, 2 * 1024)
+    assert sized(dense(L=1, H=1, D=520, B=1, S=1 << 24), 1)[0] == U
