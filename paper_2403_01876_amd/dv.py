@@ -173,10 +173,14 @@ class Cache:
         return ctypes.byref(self.c)
 
 
-def _i32(a):
+def _i32(a, n: int):
+    """An int32 array the library reads ``n`` entries of (one per sequence):
+    shorter arrays are refused here, since the C side cannot see their length."""
     if a is None:
         return None, 0
-    arr = np.ascontiguousarray(a, dtype=np.int32)
+    arr = np.ascontiguousarray(a, dtype=np.int32).reshape(-1)
+    if arr.size < n:
+        raise ValueError(f"range array has {arr.size} entries, the cache has {n} sequences")
     return arr, arr.ctypes.data
 
 
@@ -193,8 +197,8 @@ def dv_cache_bytes(cache: Cache) -> int:
 
 
 def dv_packed_bytes(cache: Cache, l0: int, l1: int, t0, t1, check: bool = True):
-    a0, p0 = _i32(t0)
-    a1, p1 = _i32(t1)
+    a0, p0 = _i32(t0, cache.c.batch)
+    a1, p1 = _i32(t1, cache.c.batch)
     out = ctypes.c_uint64(0)
     rc = lib.dv_packed_bytes(cache.ref, l0, l1, p0, p1, ctypes.byref(out))
     _check(rc, "dv_packed_bytes", check)
@@ -204,8 +208,8 @@ def dv_packed_bytes(cache: Cache, l0: int, l1: int, t0, t1, check: bool = True):
 def dv_stream_out_prompt(src: Cache, mb: int, l0: int, l1: int, t0, t1, dst, dst_cap: int,
                          stream=None, check: bool = True):
     """Returns the stream size in bytes (or ``(status, bytes)`` with check=False)."""
-    a0, p0 = _i32(t0)
-    a1, p1 = _i32(t1)
+    a0, p0 = _i32(t0, src.c.batch)
+    a1, p1 = _i32(t1, src.c.batch)
     out = ctypes.c_uint64(0)
     rc = lib.dv_stream_out_prompt(src.ref, mb, l0, l1, p0, p1, _addr(dst), dst_cap,
                                   ctypes.byref(out), _stream(stream))
@@ -215,7 +219,7 @@ def dv_stream_out_prompt(src: Cache, mb: int, l0: int, l1: int, t0, t1, dst, dst
 
 def dv_stream_out_token(src: Cache, mb: int, l0: int, l1: int, pos, dst, dst_cap: int,
                         stream=None, check: bool = True):
-    ap, pp = _i32(pos)
+    ap, pp = _i32(pos, src.c.batch)
     out = ctypes.c_uint64(0)
     rc = lib.dv_stream_out_token(src.ref, mb, l0, l1, pp, _addr(dst), dst_cap,
                                  ctypes.byref(out), _stream(stream))
@@ -225,8 +229,8 @@ def dv_stream_out_token(src: Cache, mb: int, l0: int, l1: int, pos, dst, dst_cap
 
 def dv_stream_in(dst: Cache, mb: int, l0: int, l1: int, t0, t1, src, src_bytes: int,
                  stream=None, check: bool = True) -> int:
-    a0, p0 = _i32(t0)
-    a1, p1 = _i32(t1)
+    a0, p0 = _i32(t0, dst.c.batch)
+    a1, p1 = _i32(t1, dst.c.batch)
     rc = lib.dv_stream_in(dst.ref, mb, l0, l1, p0, p1, _addr(src), src_bytes, _stream(stream))
     return _check(rc, "dv_stream_in", check)
 
@@ -235,24 +239,24 @@ def dv_block_claims(cache: Cache, mb: int, t0, t1, counts, stream=None,
                     check: bool = True) -> int:
     """Per-block claim counts of a paged table over the ranges, into the
     device int32 buffer `counts` (read it after synchronising)."""
-    a0, p0 = _i32(t0)
-    a1, p1 = _i32(t1)
+    a0, p0 = _i32(t0, cache.c.batch)
+    a1, p1 = _i32(t1, cache.c.batch)
     rc = lib.dv_block_claims(cache.ref, mb, p0, p1, _addr(counts), _stream(stream))
     return _check(rc, "dv_block_claims", check)
 
 
 def dv_swap_out(dev: Cache, slot: int, host: Cache, host_mb: int, l0: int, l1: int, t0, t1,
                 stream=None, check: bool = True) -> int:
-    a0, p0 = _i32(t0)
-    a1, p1 = _i32(t1)
+    a0, p0 = _i32(t0, dev.c.batch)
+    a1, p1 = _i32(t1, dev.c.batch)
     rc = lib.dv_swap_out(dev.ref, slot, host.ref, host_mb, l0, l1, p0, p1, _stream(stream))
     return _check(rc, "dv_swap_out", check)
 
 
 def dv_swap_in(host: Cache, host_mb: int, dev: Cache, slot: int, l0: int, l1: int, t0, t1,
                stream=None, check: bool = True) -> int:
-    a0, p0 = _i32(t0)
-    a1, p1 = _i32(t1)
+    a0, p0 = _i32(t0, host.c.batch)
+    a1, p1 = _i32(t1, host.c.batch)
     rc = lib.dv_swap_in(host.ref, host_mb, dev.ref, slot, l0, l1, p0, p1, _stream(stream))
     return _check(rc, "dv_swap_in", check)
 
@@ -272,7 +276,7 @@ class Swapper:
         self.h = h
 
     def prefetch(self, mb: int, lens, check: bool = True) -> int:
-        a, p = _i32(lens)
+        a, p = _i32(lens, self.host.c.batch)
         return _check(lib.dv_swapper_prefetch(self.h, mb, p), "dv_swapper_prefetch", check)
 
     def begin_step(self, mb: int, stream=None) -> int:
@@ -282,8 +286,8 @@ class Swapper:
         return slot.value
 
     def end_step(self, mb: int, t0, t1, stream=None, check: bool = True) -> int:
-        a0, p0 = _i32(t0)
-        a1, p1 = _i32(t1)
+        a0, p0 = _i32(t0, self.host.c.batch)
+        a1, p1 = _i32(t1, self.host.c.batch)
         return _check(lib.dv_swapper_end_step(self.h, mb, _stream(stream), p0, p1),
                       "dv_swapper_end_step", check)
 
@@ -322,8 +326,8 @@ class Streamer:
              stream=None, check: bool = True):
         """Returns the region's size in bytes (or (status, bytes) with check=False).
         ``dst_offset`` defaults to ``staging_offset``."""
-        a0, p0 = _i32(t0)
-        a1, p1 = _i32(t1)
+        a0, p0 = _i32(t0, self.src.c.batch)
+        a1, p1 = _i32(t1, self.src.c.batch)
         out = ctypes.c_uint64(0)
         if dst_offset is None:
             dst_offset = staging_offset

@@ -394,3 +394,18 @@ def test_extent_limits_at_and_past_the_boundary():
     # capacity * head_dim * elem_bytes = 2^34 bytes
     assert sized(dense(L=1, H=1, D=512, B=1, S=1 << 24), 1) == (0, 2 * 1024)
     assert sized(dense(L=1, H=1, D=520, B=1, S=1 << 24), 1)[0] == U
+
+
+def test_binding_refuses_range_arrays_shorter_than_the_batch():
+    """The library reads one range entry per sequence and cannot see an
+    array's length: the binding refuses a short one before the call."""
+    c = dense(B=4)
+    with pytest.raises(ValueError):
+        dv.dv_packed_bytes(c, 0, 2, None, np.array([1, 2, 3], np.int32))
+    with pytest.raises(ValueError):
+        dv.dv_stream_out_prompt(c, 0, 0, 2, [0, 0], np.ones(4, np.int32), FAKE + (1 << 30), 1)
+    with pytest.raises(ValueError):
+        dv.dv_stream_out_token(c, 0, 0, 2, [1, 2, 3], FAKE + (1 << 30), 1 << 20)
+    with pytest.raises(ValueError):
+        dv.dv_stream_in(c, 0, 0, 2, None, [5], FAKE + (1 << 30), 1 << 20)
+    assert dv.dv_packed_bytes(c, 0, 2, None, np.ones(4, np.int32)) == 2 * 2 * 3 * 64 * 2 * 4
