@@ -94,6 +94,11 @@ class Timer:
     def min_ms(self) -> float:
         return min(a.elapsed_time(b) for a, b in self.pairs)
 
+    def median_ms(self) -> float:
+        ts = sorted(a.elapsed_time(b) for a, b in self.pairs)
+        n = len(ts)
+        return ts[n // 2] if n % 2 else 0.5 * (ts[n // 2 - 1] + ts[n // 2])
+
 
 def flush_l2(torch, scratch):
     """Overwrite 512 MB so no payload is served from L2 / MALL."""
@@ -287,7 +292,7 @@ def S_of(w):
     return w.max_seq
 
 
-def bulk_bench(torch, dv, synth, idx, reps=10, ksplit=False):
+def bulk_bench(torch, dv, synth, idx, reps=20, ksplit=False):
     """Bulk stream-out and stream-in of one workload, timed per call (with
     ``ksplit``, the dense workload stored with the split-key layout)."""
     dev = torch.device("cuda:0")
@@ -364,7 +369,8 @@ def bulk_bench(torch, dv, synth, idx, reps=10, ksplit=False):
     for name, t in timers:
         ms = t.mean_ms()
         gbs = 2 * P / (ms * 1e-3) / 1e9
-        res[name] = {"ms": round(ms, 4), "min_ms": round(t.min_ms(), 4),
+        res[name] = {"ms": round(ms, 4), "median_ms": round(t.median_ms(), 4),
+                     "min_ms": round(t.min_ms(), 4),
                      "GBps_2x": round(gbs, 1), "payload_GBps": round(gbs / 2, 1),
                      "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
     res["cache_state"] = "cold: 512 MB written between calls"
