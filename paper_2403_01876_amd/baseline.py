@@ -33,10 +33,10 @@ def _load():
 def per_region_copy(cache: dv.Cache, mb: int, l0: int, l1: int, t0, t1, dst, dst_cap: int,
                     stream=None) -> int:
     """Returns the number of copy calls issued."""
-    a0 = np.ascontiguousarray(t0, dtype=np.int32)
-    a1 = np.ascontiguousarray(t1, dtype=np.int32)
-    n = _load().dvb_per_region_copy(cache.ref, mb, l0, l1, a0.ctypes.data, a1.ctypes.data,
-                                    dv._addr(dst), dst_cap, dv._stream(stream))
+    a0, p0 = dv._i32(np.zeros(cache.c.batch, np.int32) if t0 is None else t0, cache.c.batch)
+    a1, p1 = dv._i32(t1, cache.c.batch)
+    n = _load().dvb_per_region_copy(cache.ref, mb, l0, l1, p0, p1, dv._addr(dst), dst_cap,
+                                    dv._stream(stream))
     if n < 0:
         raise dv.DvError(int(n), "dvb_per_region_copy")
     return int(n)
