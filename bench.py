@@ -63,7 +63,8 @@ def parse():
     p.add_argument("--no-extras", action="store_true")
     p.add_argument("--extras", choices=("all", "bulk", "calib", "swap", "none"), default="all",
                    help="calib: only the known-size copy used to scale counter runs; "
-                        "bulk: the bulk workloads and that copy; swap: the OPT-66B swaps only")
+                        "bulk: the bulk workloads and that copy; swap: the OPT-66B swaps and "
+                        "the swap protocol only")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--eager", action="store_true",
                    help="report the step issued call by call instead of graph-replayed")
@@ -1154,6 +1155,8 @@ def main():
         out["calibration_d2d_copy"] = copy_calibration(torch)
     if extras == "swap":
         out["swap"] = swap_bench(torch, dv, synth)
+        out["swap_protocol"] = swap_protocol_bench(torch, dv, synth,
+                                                   out["swap"]["swap_in"]["GBps"])
     if extras == "all":
         log("extras: increments")
         out["increments"] = increments_bench(torch, dv, synth)
