@@ -1050,9 +1050,10 @@ def cpu_baseline_per_op(orc):
     return out
 
 
-def counted_traffic():
-    """HBM bytes per launch of the bulk pack kernel from the committed counter
-    summary, or None if the kernel sources changed since it was taken."""
+def counted_traffic(which: str = "traffic_bytes_per_launch"):
+    """HBM bytes per launch of the bulk pack kernel (or, with
+    ``traffic_bytes_per_launch_unpack``, the unpack kernel) from the committed
+    counter summary, or None if the kernel sources changed since it was taken."""
     import hashlib
     import re
     path = os.path.join(ROOT, "profiles", "dense_runs_hbm_traffic_opt13b_stage.md")
@@ -1061,7 +1062,7 @@ def counted_traffic():
     except OSError:
         return None
     m_sha = re.search(r"^kernel_source_sha256: ([0-9a-f]{64})$", text, re.M)
-    m_t = re.search(r"^traffic_bytes_per_launch: (\d+)$", text, re.M)
+    m_t = re.search(r"^%s: (\d+)$" % re.escape(which), text, re.M)
     if not (m_sha and m_t):
         return None
     h = hashlib.sha256()
@@ -1144,7 +1145,9 @@ def main():
         "kernels": {
             "dense_runs_kernel<unpack>": {"avg_ms": round(r["unpack_ms"], 4),
                                           "GBps_2x": round(unpack_gbs, 1),
-                                          "frac_hbm": round(unpack_gbs / HBM_PEAK_GBS, 4)},
+                                          "frac_hbm": round(unpack_gbs / HBM_PEAK_GBS, 4),
+                                          "traffic": counted_traffic(
+                                              "traffic_bytes_per_launch_unpack")},
         },
     }
     extras = "none" if args.no_extras else args.extras

@@ -19,8 +19,9 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_counted_traffic_follows_the_kernel_sources(tmp_path, monkeypatch):
-    t = bench.counted_traffic()
-    assert t is None or 2 * 1282252800 <= t <= 1.01 * 2 * 1282252800
+    for which in ("traffic_bytes_per_launch", "traffic_bytes_per_launch_unpack"):
+        t = bench.counted_traffic(which)
+        assert t is None or 2 * 1282252800 <= t <= 1.01 * 2 * 1282252800
     # a summary whose recorded hash does not match the sources gives None
     prof = tmp_path / "profiles"
     prof.mkdir()
