@@ -132,11 +132,13 @@ typedef struct dv_cache {
  * optimisation 2). */
 
 /* Storage bytes of one microbatch of `c` (dense: L*2*B*H*S*D*E; paged:
- * L*2*NB*H*bs*D*E).  Host-only.  DV_OK, DV_ERR_INVALID. */
+ * L*2*NB*H*bs*D*E).  Host-only.  DV_OK, DV_ERR_INVALID, DV_ERR_UNSUPPORTED
+ * (extents past the limits listed with DV_ERR_UNSUPPORTED). */
 DV_API int dv_cache_bytes(const dv_cache* c, uint64_t* out_bytes);
 
 /* Bytes of the contiguous buffer for these ranges (formula above).  t0 may
- * be NULL (all zero).  Host-only.  DV_OK, DV_ERR_INVALID, DV_ERR_RANGE. */
+ * be NULL (all zero).  Host-only.  DV_OK, DV_ERR_INVALID, DV_ERR_RANGE,
+ * DV_ERR_UNSUPPORTED. */
 DV_API int dv_packed_bytes(const dv_cache* c, int32_t l0, int32_t l1, const int32_t* t0,
                     const int32_t* t1, uint64_t* out_bytes);
 
@@ -150,7 +152,8 @@ DV_API int dv_packed_bytes(const dv_cache* c, int32_t l0, int32_t l1, const int3
  * DV_ERR_SPACE.  Paged caches: tokens whose table entry is outside
  * [0, num_blocks) are rejected by no host check (the table is on the
  * device); the kernel skips them and their wire bytes are left unwritten.
- * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_HIP. */
+ * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_UNSUPPORTED,
+ * DV_ERR_HIP. */
 DV_API int dv_stream_out_prompt(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
                          const int32_t* t0, const int32_t* t1, void* dst, uint64_t dst_cap,
                          uint64_t* out_bytes, void* stream);
@@ -185,7 +188,8 @@ DV_API int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int3
  * either way.  The workspace must not overlap the cache or `src`
  * (DV_ERR_INVALID); its contents are scratch between calls, and calls that
  * scatter into the same microbatch must not overlap in time.
- * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_HIP. */
+ * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_UNSUPPORTED,
+ * DV_ERR_HIP. */
 DV_API int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
                  const int32_t* t1, const void* src, uint64_t src_bytes, void* stream);
 
