@@ -1151,37 +1151,51 @@ def main():
         },
     }
     extras = "none" if args.no_extras else args.extras
+    errors = {}
+
+    def extra(key, label, fn):
+        """Run one extra measurement.  A Python-level failure (an allocation
+        refused on a box with less pinned memory, say) is recorded in the
+        line's ``errors`` and on stderr instead of losing the line."""
+        if label:
+            log(f"extras: {label}")
+        try:
+            out[key] = fn()
+        except Exception as e:  # noqa: BLE001 -- reported, not swallowed
+            errors[key] = f"{type(e).__name__}: {e}"
+            log(f"extras: {key} failed: {errors[key]}")
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+
     if extras == "calib":
-        out["calibration_d2d_copy"] = copy_calibration(torch)
+        extra("calibration_d2d_copy", "", lambda: copy_calibration(torch))
     if extras == "bulk":
-        out["bulk"] = bulk_all(torch, dv, synth)
-        out["calibration_d2d_copy"] = copy_calibration(torch)
+        extra("bulk", "", lambda: bulk_all(torch, dv, synth))
+        extra("calibration_d2d_copy", "", lambda: copy_calibration(torch))
     if extras == "swap":
-        out["swap"] = swap_bench(torch, dv, synth)
-        out["swap_protocol"] = swap_protocol_bench(torch, dv, synth,
-                                                   out["swap"]["swap_in"]["GBps"])
+        extra("swap", "swap", lambda: swap_bench(torch, dv, synth))
+        if "swap" in out:
+            extra("swap_protocol", "swap protocol", lambda: swap_protocol_bench(
+                torch, dv, synth, out["swap"]["swap_in"]["GBps"]))
     if extras == "all":
-        log("extras: increments")
-        out["increments"] = increments_bench(torch, dv, synth)
-        log("extras: tiny workload")
-        out["tiny"] = tiny_bench(torch, dv, synth)
-        out["bulk"] = bulk_all(torch, dv, synth)
-        log("extras: swap")
-        out["swap"] = swap_bench(torch, dv, synth)
-        log("extras: swap protocol")
-        out["swap_protocol"] = swap_protocol_bench(torch, dv, synth,
-                                                   out["swap"]["swap_in"]["GBps"])
-        log("extras: streaming overlapped with compute")
-        out["overlap"] = overlap_bench(torch, dv, synth)
-        log("extras: ring replication and recovery")
-        out["ring_recovery"] = ring_recovery_bench(torch, dv, synth)
-        log("extras: buffered vs per-region copies")
-        out["buffered_vs_per_region"] = buffered_vs_per_region(torch, dv, synth)
-        log("extras: copy calibration")
-        out["calibration_d2d_copy"] = copy_calibration(torch)
+        extra("increments", "increments", lambda: increments_bench(torch, dv, synth))
+        extra("tiny", "tiny workload", lambda: tiny_bench(torch, dv, synth))
+        extra("bulk", "", lambda: bulk_all(torch, dv, synth))
+        extra("swap", "swap", lambda: swap_bench(torch, dv, synth))
+        if "swap" in out:
+            extra("swap_protocol", "swap protocol", lambda: swap_protocol_bench(
+                torch, dv, synth, out["swap"]["swap_in"]["GBps"]))
+        extra("overlap", "streaming overlapped with compute",
+              lambda: overlap_bench(torch, dv, synth))
+        extra("ring_recovery", "ring replication and recovery",
+              lambda: ring_recovery_bench(torch, dv, synth))
+        extra("buffered_vs_per_region", "buffered vs per-region copies",
+              lambda: buffered_vs_per_region(torch, dv, synth))
+        extra("calibration_d2d_copy", "copy calibration", lambda: copy_calibration(torch))
     if not args.no_cpu_baseline:
-        log("cpu baseline (oracle)")
-        out["cpu_baseline"] = cpu_baseline()
+        extra("cpu_baseline", "cpu baseline (oracle)", cpu_baseline)
+    if errors:
+        out["errors"] = errors
     print(json.dumps(out), flush=True)
     failed = [k for k, v in r["checks"].items() if not v]
     for name, res in out.get("bulk", {}).items():
