@@ -19,7 +19,6 @@ below fixes the oracle to something other than its own formulas:
 ``test_planted_mistakes_are_caught`` builds the oracle with known mistakes
 planted and checks that these pins fail for every one of them.
 """
-import os
 
 import numpy as np
 import pytest
