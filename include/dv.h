@@ -177,11 +177,13 @@ DV_API int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int3
  * with an unmapped entry are skipped.  A token increment is streamed in with
  * t0 = pos, t1 = pos + 1.
  *
- * Paged receivers with a block_owner workspace for `mb`: when the call moves
- * more than one token of some sequence, has at most 64 sequences and writes
- * at least half of the pool's blocks, the library first rebuilds in the
- * workspace the inverse of the table over the streamed ranges (pool block ->
- * sequence * max_blocks + logical block, -1 for blocks not written) and then
+ * Paged receivers with a block_owner workspace for `mb`: when some
+ * sequence's run per head is longer than 4 KB (shorter runs go through a
+ * kernel that moves one 16-byte unit per lane in stream order), the call has
+ * at most 64 sequences and it writes at least half of the pool's blocks,
+ * the library first rebuilds in the workspace the inverse of the table over
+ * the streamed ranges (pool block -> sequence * max_blocks + logical block,
+ * -1 for blocks not written) and then
  * writes the pool in physical block order, so the writes are sequential
  * instead of scattered by the table (measured on MI355X: 70 % -> 74 % of HBM
  * peak for the LLaMA-2-70B stage's pool).  The bytes written are the same

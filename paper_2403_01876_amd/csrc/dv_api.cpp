@@ -25,6 +25,11 @@ using dv::kSeqPerLaunch;
 // (57 GB/s against 54 GB/s).
 constexpr int64_t kNarrowRowBytes = 64 * 1024;
 
+// Streams whose longest (sequence, head) run has at most this many 16-byte
+// units use the flattened short-run kernel; longer runs use the tiled
+// kernels, whose 512-unit tiles would otherwise leave most lanes idle.
+constexpr int64_t kSmallRunUnits = 256;
+
 // A validated view of one microbatch of a cache, sizes in 16-byte units.
 struct View {
   int kind;
@@ -150,6 +155,9 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
   int32_t max_n = 0;
   for (int32_t x : n) max_n = std::max(max_n, x);
   const bool single = max_n <= 1;
+  // Runs of at most kSmallRunUnits units per (sequence, head) go through the
+  // flattened short-run kernel instead of the tiled ones.
+  const bool small = !single && (int64_t)max_n * v.du <= kSmallRunUnits;
 
   int64_t p_group = 0;  // tokens of all earlier launch groups
   for (int64_t g0 = 0; g0 < v.B; g0 += kSeqPerLaunch) {
@@ -216,6 +224,59 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
         }
       }
       if (e != hipSuccess) return hip_fail(e, "token kernel launch");
+      continue;
+    }
+
+    if (small) {
+      dv::SmallRunArgs a;
+      memset(&a, 0, sizeof a);
+      a.cache = v.base;
+      a.wire = wire_g;
+      a.bt = v.bt;
+      a.du = (int32_t)v.du;
+      a.heads = (int32_t)v.H;
+      a.nseq = nseq;
+      a.b0 = (int32_t)g0;
+      a.r = r;
+      const int64_t units = ntok * v.H * v.du;
+      if (units >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
+      hipError_t e;
+      if (v.kind == DV_PAGED) {
+        a.paged = 1;
+        a.block_size = (int32_t)v.bs;
+        a.num_blocks = (int32_t)v.NB;
+        a.max_blocks = (int32_t)v.max_blocks;
+        a.s_slab = v.NB * v.H * v.bs * v.du;
+        a.s_blk = v.H * v.bs * v.du;
+        a.s_h = v.bs * v.du;
+        a.s_tok = v.du;
+        a.s_e = 1;
+        a.m = {2 * l0, 1, 0, 0, w_slab};
+        e = dv::launch_small_runs(dir, a, (uint32_t)units, 2 * nl, st);
+      } else {
+        a.s_slab = v.B * v.H * v.S * v.du;
+        a.s_b = v.H * v.S * v.du;
+        a.s_h = v.S * v.du;
+        if (v.kind == DV_DENSE) {
+          a.s_tok = v.du;
+          a.s_e = 1;
+          a.m = {2 * l0, 1, 0, 0, w_slab};
+          e = dv::launch_small_runs(dir, a, (uint32_t)units, 2 * nl, st);
+        } else {
+          // split key slabs: groups S units apart, tokens 1 unit apart
+          a.s_tok = 1;
+          a.s_e = v.S;
+          a.m = {2 * l0, 2, 0, 0, w_slab};
+          e = dv::launch_small_runs(dir, a, (uint32_t)units, nl, st);
+          if (e == hipSuccess) {
+            a.s_tok = v.du;
+            a.s_e = 1;
+            a.m = {2 * l0 + 1, 2, 1, 0, w_slab};
+            e = dv::launch_small_runs(dir, a, (uint32_t)units, nl, st);
+          }
+        }
+      }
+      if (e != hipSuccess) return hip_fail(e, "short-run kernel launch");
       continue;
     }
 

@@ -93,6 +93,29 @@ struct TokenArgs {
   int32_t pos[kSeqPerLaunch];  // token of each sequence, < 0 = inactive
 };
 
+// Short runs (a few tokens per sequence, e.g. a decode step that accepts
+// several tokens): one 16-byte unit per lane over the flattened wire order
+// of each slab, (sequence, head, token, unit), so no lane idles the way it
+// would in a tile sized for long runs.  Unit e of sequence b's run for head
+// h holds token t0 + e / du, group e % du, at cache offset
+// (t0 + e / du) * s_tok + (e % du) * s_e from the (sequence, head) base;
+// paged caches find the token's block through the table.
+struct SmallRunArgs {
+  void* cache;
+  void* wire;
+  const int32_t* bt;  // paged only
+  int64_t s_slab;
+  int64_t s_b;        // dense: units per sequence
+  int64_t s_blk;      // paged: units per block
+  int64_t s_h;        // units per head
+  int64_t s_tok;      // units per token (du, or 1 in a split key slab)
+  int64_t s_e;        // units between consecutive 16-byte groups of a token (1, or S)
+  SlabMap m;
+  int32_t du, heads, nseq, b0;
+  int32_t paged, block_size, num_blocks, max_blocks;
+  SeqRanges r;
+};
+
 // Split-key slab: 64-token tiles transposed through LDS.
 struct KsplitArgs {
   void* cache;
@@ -136,6 +159,8 @@ hipError_t launch_owner_map(const OwnerArgs& a, hipStream_t s);
 hipError_t launch_block_claims(const OwnerArgs& a, bool clear, hipStream_t s);
 hipError_t launch_token(int dir, const TokenArgs& a, uint32_t units_per_slab, uint32_t nslabs,
                         hipStream_t s);
+hipError_t launch_small_runs(int dir, const SmallRunArgs& a, uint32_t units_per_slab,
+                             uint32_t nslabs, hipStream_t s);
 hipError_t launch_ksplit(int dir, const KsplitArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,
                          hipStream_t s);
 hipError_t launch_copy(const CopyArgs& a, uint32_t units_per_slab, uint32_t nslabs, hipStream_t s);

@@ -289,6 +289,76 @@ __global__ void __launch_bounds__(kThreads) token_kernel(TokenArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Short runs: grid (ceil(units_per_slab / (256 * U)), nslabs).  Each lane
+// moves U wire units of the flattened (sequence, head, token, unit) order
+// of its slab, 256 units apart; the per-sequence prefix of run sizes sits in
+// LDS and a 6-step binary search names each unit's sequence (the
+// single-token kernel above skips the search, since there every run is one
+// token).  Loads are clamped to the last unit and issue before any store.
+// ---------------------------------------------------------------------------
+template <int D, int U>
+__global__ void __launch_bounds__(kThreads) small_runs_kernel(SmallRunArgs a) {
+  __shared__ int s_incl[kSeqPerLaunch];  // inclusive prefix of n_b * heads * du
+  __shared__ int s_run[kSeqPerLaunch];   // n_b * du: units per head of sequence b
+  __shared__ int s_t0[kSeqPerLaunch];
+  const int lane = lane_id();
+  if (threadIdx.x < 64) {
+    int n = 0, t0 = 0;
+    if (lane < a.nseq) {
+      n = a.r.n[lane];
+      t0 = a.r.t0[lane];
+    }
+    s_incl[lane] = wave_incl_scan(n * a.heads * a.du);
+    s_run[lane] = n * a.du;
+    s_t0[lane] = t0;
+  }
+  __syncthreads();
+  const int total = s_incl[kSeqPerLaunch - 1];
+  const int64_t y = blockIdx.y;
+  const int64_t slab = a.m.slab0 + y * a.m.slab_step;
+  const int64_t wslab = a.m.wslab0 + y * a.m.slab_step;
+  u32x4* cache_slab = (u32x4*)a.cache + slab * a.s_slab;
+  u32x4* wire_slab = (u32x4*)a.wire + wslab * a.m.w_slab;
+  int64_t co[U];
+  bool ok[U];
+  u32x4 v[U];
+#pragma unroll
+  for (int i = 0; i < U; ++i) {
+    const int u0 = (blockIdx.x * U + i) * kThreads + threadIdx.x;
+    const int u = min(u0, total - 1);
+    // The first sequence whose inclusive prefix exceeds u (it has n_b > 0).
+    int lo = 0, hi = kSeqPerLaunch - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (s_incl[mid] > u) hi = mid; else lo = mid + 1;
+    }
+    const int b = lo;
+    const int run = s_run[b];
+    const int rem = u - (s_incl[b] - run * a.heads);
+    const int h = rem / run;
+    const int e = rem - h * run;  // unit within the (sequence, head) run
+    const int t = e / a.du;
+    const int g = e - t * a.du;   // 16-byte group within the token
+    const int s = s_t0[b] + t;    // token position in the cache
+    ok[i] = u0 < total;
+    if (!a.paged) {
+      co[i] = (int64_t)(a.b0 + b) * a.s_b + (int64_t)s * a.s_tok;
+    } else {
+      const int blk = a.bt[(int64_t)(a.b0 + b) * a.max_blocks + s / a.block_size];
+      ok[i] = ok[i] && blk >= 0 && blk < a.num_blocks;  // unmapped block: skipped
+      co[i] = (int64_t)(ok[i] ? blk : 0) * a.s_blk + (int64_t)(s % a.block_size) * a.s_tok;
+    }
+    co[i] += (int64_t)h * a.s_h + (int64_t)g * a.s_e;
+    v[i] = ld_nt((D == kPack) ? cache_slab + co[i] : wire_slab + u);
+  }
+#pragma unroll
+  for (int i = 0; i < U; ++i) {
+    const int u = (blockIdx.x * U + i) * kThreads + threadIdx.x;
+    if (ok[i]) st_nt(v[i], (D == kPack) ? wire_slab + u : cache_slab + co[i]);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Split-key slab: grid (tiles_per_slab, nslabs); a tile is 64 tokens of one
 // (sequence, head).  The cache holds the head as [group][token] (each group
 // 16 bytes), the wire as [token][group]: the tile is read with lanes along
@@ -486,6 +556,22 @@ hipError_t launch_token(int dir, const TokenArgs& a, uint32_t units_per_slab, ui
   const void* fn =
       dir == kPack ? (const void*)&token_kernel<kPack> : (const void*)&token_kernel<kUnpack>;
   return launch(fn, dim3((units_per_slab + kThreads - 1) / kThreads, nslabs), a, s);
+}
+
+hipError_t launch_small_runs(int dir, const SmallRunArgs& a, uint32_t units_per_slab,
+                             uint32_t nslabs, hipStream_t s) {
+  // Two units per lane once a launch moves 8 MB or more; measured on MI355X
+  // for 2-16 tokens per sequence, one unit per lane is faster below that
+  // (fewer dependent steps per lane) and two above (fewer workgroups).
+  const bool two = (uint64_t)units_per_slab * nslabs >= (1ull << 19);
+  const void* fn;
+  if (dir == kPack)
+    fn = two ? (const void*)&small_runs_kernel<kPack, 2> : (const void*)&small_runs_kernel<kPack, 1>;
+  else
+    fn = two ? (const void*)&small_runs_kernel<kUnpack, 2>
+             : (const void*)&small_runs_kernel<kUnpack, 1>;
+  const uint32_t per = kThreads * (two ? 2 : 1);
+  return launch(fn, dim3((units_per_slab + per - 1) / per, nslabs), a, s);
 }
 
 hipError_t launch_ksplit(int dir, const KsplitArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,

@@ -122,8 +122,11 @@ def test_paged_unmapped_entries_are_skipped(oracle_lib):
 
     Expected values come from the oracle over a pool with one extra block per
     (layer, K|V) slab that the invalid entries are pointed at: filled with the
-    wire sentinel for pack, and dropped again after unpack."""
-    L, H, D, B, E, bs = 2, 2, 64, 3, 2, 4
+    wire sentinel for pack, and dropped again after unpack.  Three range
+    shapes reach the three paged paths: runs longer than 4 KB per head (tiled
+    kernel, pool order with the workspace), single tokens, and runs of 4 KB
+    (short-run kernel)."""
+    L, H, D, B, E, bs = 2, 2, 512, 3, 2, 4
     bt = np.array([[0, 1, 2], [3, -1, 4], [5, 99, 6]], np.int32)
     nb = 7
     blk = H * bs * D * E  # bytes per block per slab
@@ -145,13 +148,17 @@ def test_paged_unmapped_entries_are_skipped(oracle_lib):
     btd = G.to_dev(bt)
     c = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool], block_size=bs, num_blocks=nb, max_blocks=3,
                  block_tables=[btd])
-    for single in (False, True):
+    for case in ("long", "single", "short"):
+        single = case == "single"
         if single:
             t0 = np.array([5, 5, 5], np.int32)  # logical block 1 of each sequence
             t1 = t0 + 1
-        else:
+        elif case == "long":
             t0 = np.array([0, 1, 2], np.int32)
             t1 = np.array([12, 9, 11], np.int32)
+        else:  # 4 tokens x 64 units = 4 KB per head, across the unmapped entries
+            t0 = np.array([2, 3, 4], np.int32)
+            t1 = t0 + 4
         n = dv.dv_packed_bytes(c, 0, L, t0, t1)
         wire = G.dev_const(n, 0x5C)
         if single:
@@ -179,8 +186,10 @@ def test_paged_unmapped_entries_are_skipped(oracle_lib):
         dv.dv_stream_in(rc2, 0, 0, L, t0, t1, G.to_dev(wh), n, stream())
         torch.cuda.synchronize()
         assert G.host(recv2).tobytes() == drop_extra(exp_pool).tobytes()
-        if not single:  # 9 logical blocks streamed, 7 pool blocks: pool order taken
+        if case == "long":  # 9 logical blocks streamed, 7 pool blocks: pool order taken
             assert G.host(ws).view(np.int32).tolist() == [0, 1, 2, 3, 5, 6, 8]
+        else:  # token and short-run kernels scatter in stream order
+            assert (G.host(ws) == 0x7E).all()
 
 
 def test_graph_replay_paged_pool_order_and_split_key(oracle_lib):

@@ -3,8 +3,8 @@
 Each case draws a sender and a receiver layout independently (dense, paged
 or split key, each with its own capacity, block size and table), shared
 layer / head / head_dim / batch / element-size extents, a layer sub-range
-and per-sequence ranges (prompt prefixes, arbitrary spans, empty ranges,
-single tokens with inactive sequences), then packs the sender, compares the
+and per-sequence ranges (prompt prefixes, arbitrary spans, runs of a few
+tokens, empty ranges, single tokens with inactive sequences), then packs the sender, compares the
 stream with the oracle's pack, streams it into a sentinel-filled receiver
 (paged receivers sometimes with an owner-map workspace) and compares the
 whole receiver with the oracle's unpack.  Every case prints its seed first,
@@ -71,7 +71,7 @@ def one_case(orc, seed):
     B = int(r.integers(65, 90)) if r.random() < 0.1 else int(r.integers(1, 10))
     kinds = [int(k) for k in r.choice(KINDS, size=2)]
     tmax = int(r.integers(1, 160))
-    style = r.choice(["prompt", "spans", "tokens"])
+    style = r.choice(["prompt", "spans", "tokens", "short"])
     if style == "tokens":
         pos = r.integers(0, tmax, size=B).astype(np.int32)
         pos[r.random(B) < 0.3] = -1
@@ -83,6 +83,9 @@ def one_case(orc, seed):
         for b in range(B):
             if style == "prompt":
                 a, c = 0, int(r.integers(0, tmax + 1))
+            elif style == "short":  # a few tokens, as a multi-token decode step
+                a = int(r.integers(0, tmax + 1))
+                c = min(tmax, a + int(r.integers(0, 13)))
             else:
                 a, c = sorted(int(v) for v in r.integers(0, tmax + 1, size=2))
             if r.random() < 0.15:

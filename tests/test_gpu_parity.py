@@ -178,7 +178,7 @@ def test_paged_gather_scatter(oracle_lib, seed):
 def test_paged_scatter_pool_order(oracle_lib, seed):
     """Scatter with an owner-map workspace: the pool equals the oracle's
     unpack whichever order the library picks; when the header's conditions
-    hold (more than one token of some sequence, at most 64 sequences, at
+    hold (some run longer than 256 16-byte units, at most 64 sequences, at
     least half of the pool's blocks written) the workspace holds the owner
     map afterwards, otherwise it is untouched.  A second call with another
     table reuses the stale workspace."""
@@ -219,7 +219,11 @@ def test_paged_scatter_pool_order(oracle_lib, seed):
         oracle_lib.unpack(lay_b, exp_recv, l0, l1, t0, t1, wire_h)
         assert G.host(recv)[: lay_b.storage_bytes()].tobytes() == exp_recv.tobytes()
         blocks = sum((t1[b] + bs - 1) // bs - t0[b] // bs for b in range(B) if t1[b] > t0[b])
-        pool_order = n > 0 and B <= 64 and (t1 - t0).max() > 1 and 2 * blocks >= nb
+        du = D * E // 16
+        # runs of at most 256 units per (sequence, head) take the short-run
+        # kernel, which scatters in stream order
+        pool_order = (n > 0 and B <= 64 and (t1 - t0).max() > 1 and
+                      (t1 - t0).max() * du > 256 and 2 * blocks >= nb)
         w = G.host(ws)
         assert (w[nb * 4:] == 0x7E).all(), "wrote past the workspace"
         if pool_order:
@@ -417,3 +421,67 @@ def test_device_fill_equals_host_fill():
         synth.device_fill(t.data_ptr(), nbytes, 0xC0FFEE, first_byte=first)
         torch.cuda.synchronize()
         assert G.host(t).tobytes() == synth.fill_bytes(nbytes, 0xC0FFEE, first_byte=first).tobytes()
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_short_runs(oracle_lib, seed):
+    """Ranges of 0 to 20 tokens per sequence -- a decode step that accepts
+    several tokens, or replication batched over a few steps -- through the
+    short-run kernel (longest run at most 256 16-byte units) and, for some
+    seeds, just past that limit through the tiled kernels.  Dense, paged and
+    split-key senders and receivers, 1/2/4-byte elements, more than 64
+    sequences for some seeds; pack and sentinel-receiver unpack against the
+    oracle byte for byte."""
+    r = np.random.default_rng(2500 + seed)
+    E = int(r.choice([2, 2, 1, 4]))
+    du = int(r.choice([1, 2, 8, 16, 32]))
+    D = du * 16 // E
+    L = int(r.integers(1, 4))
+    H = int(r.integers(1, 9))
+    B = int(r.integers(65, 80)) if seed % 6 == 5 else int(r.integers(1, 10))
+    kinds = [(dv.DV_DENSE, oracle.DENSE), (dv.DV_PAGED, oracle.PAGED),
+             (dv.DV_DENSE_KSPLIT, oracle.KSPLIT)]
+    kind, okind = kinds[seed % 3]
+    rkind, rokind = kinds[(seed // 3) % 3]
+    limit = 256 // du  # longest run (tokens) the short-run kernel takes
+    nmax = limit + 1 if seed % 4 == 3 else min(20, limit)
+    S = max(64, nmax + 8)
+    t0 = r.integers(0, S - nmax, size=B).astype(np.int32)
+    n = r.integers(0, nmax + 1, size=B).astype(np.int32)
+    n[r.random(B) < 0.2] = 0
+    if seed % 4 == 3:
+        n[int(r.integers(0, B))] = nmax  # one run just past the limit
+    t1 = (t0 + n).astype(np.int32)
+    l0 = int(r.integers(0, L))
+    l1 = int(r.integers(l0 + 1, L + 1))
+
+    def layout(k, ok, sd, fill):
+        if k == dv.DV_PAGED:
+            bs = int(r.choice([1, 4, 16]))
+            maxb = -(-S // bs)
+            bt, nb = synth.make_paged_tables(sd, [maxb * bs] * B, bs, maxb)
+            lay = oracle.Layout(ok, L, H, D, B, elem_bytes=E, block_size=bs, num_blocks=nb,
+                                block_table=bt)
+            host = synth.fill_bytes(lay.storage_bytes(), sd) if fill is None else \
+                np.full(lay.storage_bytes(), fill, np.uint8)
+            dev = G.to_dev(host)
+            desc = dv.Cache(k, L, H, D, B, [dev], elem_bytes=E, block_size=bs, num_blocks=nb,
+                            max_blocks=maxb, block_tables=[G.to_dev(bt)])
+        else:
+            lay = oracle.Layout(ok, L, H, D, B, seq_cap=S, elem_bytes=E)
+            host = synth.fill_bytes(lay.storage_bytes(), sd) if fill is None else \
+                np.full(lay.storage_bytes(), fill, np.uint8)
+            dev = G.to_dev(host)
+            desc = dv.Cache(k, L, H, D, B, [dev], max_seq=S, elem_bytes=E)
+        return lay, host, dev, desc
+
+    lay, host, dev, desc = layout(kind, okind, seed, None)
+    exp = oracle_lib.pack(lay, host, l0, l1, t0, t1)
+    got = run_pack(desc, l0, l1, t0, t1, exp.nbytes)
+    assert got.tobytes() == exp.tobytes()
+    rlay, rhost, rdev, rdesc = layout(rkind, rokind, seed + 77, 0xA5)
+    if exp.nbytes:
+        dv.dv_stream_in(rdesc, 0, l0, l1, t0, t1, G.to_dev(exp), exp.nbytes, stream())
+    torch.cuda.synchronize()
+    oracle_lib.unpack(rlay, rhost, l0, l1, t0, t1, exp)
+    assert G.host(rdev)[: rlay.storage_bytes()].tobytes() == rhost.tobytes()

@@ -240,3 +240,49 @@ def test_llama_paged_gather_scatter_and_tail_increments(oracle_lib):
     torch.cuda.synchronize()
     assert torch.equal(ga, gb)
     G.check_pack_sampled(oracle_lib, la, w.data_seed, ga, 0, L, t0, full, NSAMP, 8)
+
+
+@pytest.mark.parametrize("K", [2, 4, 8, 16])
+def test_multi_token_steps(oracle_lib, K):
+    """Decode steps that each add K tokens per sequence (speculative decoding
+    accepting several tokens, or replication batched over K steps) on the
+    OPT-13B stage and the LLaMA-2-70B paged pool, as the short-run kernel
+    moves them (one unit per lane below 8 MB a launch, two above): sampled
+    wire elements against the oracle, then stream-in into a receiver checked
+    on the device."""
+    for idx in (1, 4):
+        w = synth.make_workload(idx)
+        L, H, D, B, E = w.layers, w.heads, w.head_dim, w.batch, w.elem_bytes
+        p = w.step_positions(0).astype(np.int32)
+        t0, t1 = p, (p + K).astype(np.int32)
+        if w.paged:
+            lay = oracle.Layout(oracle.PAGED, L, H, D, B, elem_bytes=E, block_size=w.block_size,
+                                num_blocks=w.num_blocks, block_table=w.block_table_a)
+            src = G.dev_filled(lay.storage_bytes(), w.data_seed)
+            bta = G.to_dev(w.block_table_a)
+            cs = dv.Cache(dv.DV_PAGED, L, H, D, B, [src], block_size=w.block_size,
+                          num_blocks=w.num_blocks, max_blocks=w.max_blocks, block_tables=[bta])
+            recv = G.dev_const(lay.storage_bytes(), 0xA5)
+            cr = dv.Cache(dv.DV_PAGED, L, H, D, B, [recv], block_size=w.block_size,
+                          num_blocks=w.num_blocks, max_blocks=w.max_blocks, block_tables=[bta])
+        else:
+            lay = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=w.max_seq, elem_bytes=E)
+            src = G.dev_filled(lay.storage_bytes(), w.data_seed)
+            cs = dv.Cache(dv.DV_DENSE, L, H, D, B, [src], max_seq=w.max_seq)
+            recv = G.dev_const(lay.storage_bytes(), 0xA5)
+            cr = dv.Cache(dv.DV_DENSE, L, H, D, B, [recv], max_seq=w.max_seq)
+        n = dv.dv_packed_bytes(cs, 0, L, t0, t1)
+        wire = torch.empty(n, dtype=torch.uint8, device=G.DEV)
+        assert dv.dv_stream_out_prompt(cs, 0, 0, L, t0, t1, wire, n, stream()) == n
+        torch.cuda.synchronize()
+        G.check_pack_sampled(oracle_lib, lay, w.data_seed, wire, 0, L, t0, t1, 1 << 16, K)
+        dv.dv_stream_in(cr, 0, 0, L, t0, t1, wire, n, stream())
+        again = torch.empty_like(wire)
+        dv.dv_stream_out_prompt(cr, 0, 0, L, t0, t1, again, n, stream())
+        torch.cuda.synchronize()
+        assert torch.equal(again, wire)
+        if not w.paged:  # and nothing else of the receiver changed
+            G.assert_dense_ranges_equal(recv, src, L, B, H, w.max_seq, D, E, 0, L, t0, t1,
+                                        sentinel=0xA5)
+        del src, recv, wire, again
+        torch.cuda.empty_cache()
