@@ -281,14 +281,18 @@ DV_API int dv_swapper_destroy(dv_swapper* s);
  * (Sec. 4.1.1, optimisations 2 and 3).  The compute thread calls
  * dv_streamer_push after queuing the work that produces a region on its
  * compute stream; push records an event there and returns.  A worker thread
- * then, on the streamer's own stream and after that event: packs the region
+ * waits for that event on the host (no cross-stream wait is queued on the
+ * GPU) and then, on the streamer's own stream: packs the region
  * (layers [l0, l1), tokens [t0[b], t1[b]) of microbatch `mb` of `src`, t0 may
  * be NULL) into `staging` + staging_offset with dv_stream_out_prompt, and
  * copies the packed bytes to `dst` + dst_offset (pinned host memory, or
- * device memory).  Offsets are the caller's: pushing a prompt's layers one
- * by one at offsets that accumulate their sizes leaves the whole prompt's
- * contiguous buffer in `dst`, since layer ranges concatenate; decode steps
- * can cycle through a few staging slots while filling a long host log.
+ * device memory; a host destination is written by pitched copies, which run
+ * on the SDMA engines and leave the compute units to the compute stream,
+ * where a plain copy would run as a blit kernel on them).  Offsets are the
+ * caller's: pushing a prompt's layers one by one at offsets that accumulate
+ * their sizes leaves the whole prompt's contiguous buffer in `dst`, since
+ * layer ranges concatenate; decode steps can cycle through a few staging
+ * slots while filling a long host log.
  * Pushes run in push order.  `staging` (device) and `dst` are caller owned,
  * disjoint from each other and from the source microbatch (create returns
  * DV_ERR_INVALID otherwise); offsets 16-byte aligned, each must hold its

@@ -30,6 +30,9 @@ def test_layer_by_layer_prompt_to_host(oracle_lib):
     host = torch.full((total,), 0x11, dtype=torch.uint8, pin_memory=True)
     layer_wires = [synth.fill_bytes(dv.dv_packed_bytes(c, l, l + 1, zero, lens), 10 + l)
                    for l in range(L)]
+    # a host destination is written in 256 KiB rows plus a remainder: each
+    # layer here is two whole rows and a tail
+    assert all(w.size // (256 << 10) == 2 and w.size % (256 << 10) for w in layer_wires)
     dev_wires = [G.to_dev(wl) for wl in layer_wires]
     torch.cuda.synchronize()
     compute = torch.cuda.Stream()
