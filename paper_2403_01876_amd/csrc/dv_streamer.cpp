@@ -59,7 +59,7 @@ struct dv_streamer {
   hipEvent_t events[kEventPool] = {};
   std::vector<int> free_events;
   std::deque<Request> queue;
-  int busy = 0;  // requests taken by the worker and not yet enqueued
+  int busy = 0;  // requests taken by the worker and not yet complete
   int error = DV_OK;
   bool stop = false;
   std::mutex m;
