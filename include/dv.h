@@ -68,7 +68,9 @@ typedef enum {
                               capacity (max_seq, or max_blocks*block_size) above 2^24,
                               head_dim*elem_bytes above 2^20 bytes, num_heads*head_dim*
                               elem_bytes above 2^24 bytes, capacity*head_dim*elem_bytes above
-                              2^34 bytes, or a launch of 2^31 or more workgroups */
+                              2^34 bytes, or a launch whose grid would count 2^31 or more
+                              tiles or 16-byte units (each launch covers up to 64
+                              sequences; every launch of a call is checked first) */
   DV_ERR_HIP = -5          /* the HIP runtime refused to enqueue the work */
 } dv_status;
 

@@ -159,6 +159,30 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
   // flattened short-run kernel instead of the tiled ones.
   const bool small = !single && (int64_t)max_n * v.du <= kSmallRunUnits;
 
+  // Every launch group's grid, checked before anything is enqueued so that a
+  // refusal leaves the stream untouched.  Single tokens need no check: at
+  // most 64 * heads * du < 2^26 units per launch.
+  if (!single) {
+    const int64_t ngrp = (v.H + dv::kPagedHeads - 1) / dv::kPagedHeads;
+    for (int64_t g0 = 0; g0 < v.B; g0 += kSeqPerLaunch) {
+      const int64_t g1 = std::min<int64_t>(g0 + kSeqPerLaunch, v.B);
+      int64_t grid = 0, ktiles = 0;
+      for (int64_t b = g0; b < g1; ++b) {
+        const int64_t a = t0[b], k = n[b];
+        if (k == 0) continue;
+        if (small)
+          grid += k * v.H * v.du;
+        else if (v.kind == DV_PAGED)
+          grid += ((a + k + v.bs - 1) / v.bs - a / v.bs) * ngrp;
+        else
+          grid += v.H * ((k * v.du + dv::kDenseTile - 1) / dv::kDenseTile);
+        ktiles += v.H * ((k + dv::kKsplitTile - 1) / dv::kKsplitTile);
+      }
+      if (!small && v.kind == DV_DENSE_KSPLIT) grid = std::max(grid, ktiles);
+      if (grid >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
+    }
+  }
+
   int64_t p_group = 0;  // tokens of all earlier launch groups
   for (int64_t g0 = 0; g0 < v.B; g0 += kSeqPerLaunch) {
     const int nseq = (int)std::min<int64_t>(kSeqPerLaunch, v.B - g0);
@@ -238,8 +262,7 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
       a.nseq = nseq;
       a.b0 = (int32_t)g0;
       a.r = r;
-      const int64_t units = ntok * v.H * v.du;
-      if (units >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
+      const int64_t units = ntok * v.H * v.du;  // below 2^31: checked above
       hipError_t e;
       if (v.kind == DV_PAGED) {
         a.paged = 1;
@@ -322,9 +345,8 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
         const hipError_t e = dv::launch_owner_map(o, st);
         if (e != hipSuccess) return hip_fail(e, "owner map launch");
         a.owner = v.owner;
-        tiles = v.NB * ngrp;
+        tiles = v.NB * ngrp;  // below 2^31 by the condition above
       }
-      if (tiles >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
       const hipError_t e = dv::launch_paged(dir, a, (uint32_t)tiles, 2 * nl, st);
       if (e != hipSuccess) return hip_fail(e, "paged kernel launch");
       continue;
@@ -345,7 +367,6 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
     int64_t tiles = 0;
     for (int i = 0; i < nseq; ++i)
       tiles += v.H * (((int64_t)r.n[i] * v.du + dv::kDenseTile - 1) / dv::kDenseTile);
-    if (tiles >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
     if (v.kind == DV_DENSE) {
       a.m = {2 * l0, 1, 0, 0, w_slab};
       const hipError_t e = dv::launch_dense_runs(dir, a, (uint32_t)tiles, 2 * nl, st);
@@ -434,6 +455,13 @@ int swap_copy(const dv_cache* from, int32_t from_mb, const dv_cache* to, int32_t
     // Narrow rows (a decode step's update): one kernel copies them straight
     // between the slot and the pinned mirror; DMA would take one descriptor
     // per row (or one call per row block when the ranges are ragged).
+    // Every launch group's grid is checked before anything is enqueued.
+    for (int64_t g0 = 0; g0 < a.B; g0 += kSeqPerLaunch) {
+      int64_t units = 0;
+      for (int64_t b = g0; b < std::min<int64_t>(g0 + kSeqPerLaunch, a.B); ++b)
+        units += (int64_t)rn[b] * a.H * a.du;
+      if (units >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
+    }
     const uint32_t nl = (uint32_t)(l1 - l0);
     for (int64_t g0 = 0; g0 < a.B; g0 += kSeqPerLaunch) {
       const int nseq = (int)std::min<int64_t>(kSeqPerLaunch, a.B - g0);
@@ -446,7 +474,6 @@ int swap_copy(const dv_cache* from, int32_t from_mb, const dv_cache* to, int32_t
         units += (int64_t)rn[g0 + i] * a.H * a.du;
       }
       if (units == 0) continue;
-      if (units >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
       k.src = a.base;
       k.dst = b.base;
       k.s_slab = a.B * a.H * a.S * a.du;

@@ -409,3 +409,43 @@ def test_binding_refuses_range_arrays_shorter_than_the_batch():
     with pytest.raises(ValueError):
         dv.dv_stream_in(c, 0, 0, 2, None, [5], FAKE + (1 << 30), 1 << 20)
     assert dv.dv_packed_bytes(c, 0, 2, None, np.ones(4, np.int32)) == 2 * 2 * 3 * 64 * 2 * 4
+
+
+def test_oversized_later_launch_group_is_refused_before_any_launch():
+    """With more than 64 sequences a call runs in launch groups.  When only a
+    later group's grid passes 2^31 units or tiles the call must still refuse
+    before enqueuing the earlier groups: here it returns
+    DV_ERR_UNSUPPORTED, where a launch attempt (no GPU in this process)
+    would have returned DV_ERR_HIP."""
+    U = dv.DV_ERR_UNSUPPORTED
+    H, B = 1 << 20, 128
+    z = np.zeros(B, np.int32)
+    wire = 1 << 48  # far from every fake cache below
+
+    def lens(small, large):
+        return np.array([small] * 64 + [large] * 64, np.int32)
+
+    def both_directions(c, t1):
+        n = dv.dv_packed_bytes(c, 0, 1, z, t1)
+        assert dv.dv_stream_out_prompt(c, 0, 0, 1, z, t1, wire, n, check=False)[0] == U
+        assert dv.dv_stream_in(c, 0, 0, 1, z, t1, wire, n, check=False) == U
+
+    # short runs: 64 sequences x 32 tokens x 2^20 heads = 2^31 units
+    both_directions(dense(L=1, H=H, D=8, B=B, S=64), lens(1, 32))
+    # dense tiles: 64 x 2^20 heads x 32 tiles of 512 units
+    both_directions(dense(L=1, H=H, D=8, B=B, S=1 << 14), lens(1, 1 << 14))
+    # split key: the key slabs' 64-token tiles pass 2^31 (the value slabs'
+    # 512-unit tiles do not)
+    both_directions(dense(L=1, H=H, D=8, B=B, S=2048, kind=dv.DV_DENSE_KSPLIT),
+                    lens(1, 2048))
+    # paged: 64 x 64 blocks x 2^19 head pairs
+    pg = dv.Cache(dv.DV_PAGED, 1, H, 8, B, [FAKE], block_size=16, num_blocks=B * 64,
+                  max_blocks=64, block_tables=[FAKE + (1 << 46)])
+    both_directions(pg, lens(1, 1024))
+    # swap of narrow rows through the copy kernel: 64 x 32 x 2^20 units
+    dev_c = dense(L=1, H=H, D=8, B=B, S=64)
+    host_c = dense(L=1, H=H, D=8, B=B, S=64, bases=(1 << 44,), mem=dv.DV_MEM_HOST_PINNED)
+    assert dv.dv_swap_out(dev_c, 0, host_c, 0, 0, 1, z, lens(1, 32), check=False) == U
+    assert dv.dv_swap_in(host_c, 0, dev_c, 0, 0, 1, z, lens(1, 32), check=False) == U
+    # just below the limit the sizing still works: 31 tokens in the later group
+    assert dv.dv_packed_bytes(dense(L=1, H=H, D=8, B=B, S=64), 0, 1, z, lens(1, 31)) > 0
