@@ -68,7 +68,9 @@ typedef enum {
                               capacity (max_seq, or max_blocks*block_size) above 2^24,
                               head_dim*elem_bytes above 2^20 bytes, num_heads*head_dim*
                               elem_bytes above 2^24 bytes, capacity*head_dim*elem_bytes above
-                              2^34 bytes, or a launch whose grid would count 2^31 or more
+                              2^34 bytes, a cache whose storage, or whose stream of every
+                              layer and sequence at full capacity, reaches 2^48 bytes,
+                              or a launch whose grid would count 2^31 or more
                               tiles or 16-byte units (each launch covers up to 64
                               sequences; every launch of a call is checked first) */
   DV_ERR_HIP = -5          /* the HIP runtime refused to enqueue the work */
@@ -114,7 +116,10 @@ typedef struct dv_cache {
   void* const* mb_base;              /* host array [num_mb] of cache base addresses */
   const int32_t* const* block_table; /* paged: host array [num_mb] of device addresses of
                                         int32 [batch][max_blocks] tables; an entry outside
-                                        [0, num_blocks) marks an unmapped block */
+                                        [0, num_blocks) marks an unmapped block.  A table
+                                        must not overlap anything a call writes (stream
+                                        destination, pool on stream-in, owner map, claim
+                                        counts): DV_ERR_INVALID */
   int32_t* const* block_owner;       /* paged, optional (NULL, or NULL entries, to leave
                                         unused): host array [num_mb] of device addresses of
                                         caller-owned int32 [num_blocks] workspaces, 4-byte

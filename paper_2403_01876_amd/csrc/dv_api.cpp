@@ -85,6 +85,14 @@ int layout_of(const dv_cache* c, View* v) {
   if (v->cap > (1 << 24) || v->du > (1 << 16) || v->H * v->du > (1 << 20) ||
       v->cap * v->du > (1ll << 30))
     return DV_ERR_UNSUPPORTED;
+  // Every byte count derived from the descriptor stays far inside 64 bits:
+  // its storage and the longest stream it can produce (all layers, every
+  // sequence at full capacity) must be below 2^48 bytes.
+  using u128 = unsigned __int128;
+  const u128 per_token = (u128)v->L * 2 * v->H * v->du * 16;
+  const u128 rows = c->kind == DV_PAGED ? (u128)v->NB * v->bs : (u128)v->B * v->S;
+  const u128 limit = (u128)1 << 48;
+  if (per_token * rows >= limit || per_token * v->B * v->cap >= limit) return DV_ERR_UNSUPPORTED;
   v->base = nullptr;
   return DV_OK;
 }
@@ -144,6 +152,12 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 int hip_status(hipError_t e) { return hip_fail(e, "hipMemcpy2DAsync"); }
+
+// Whether [p, p + n) overlaps a paged view's block table, which the kernels
+// read while the call writes: the table must stay out of everything written.
+bool overlaps_table(const View& v, const void* p, uint64_t n) {
+  return v.bt && overlaps(p, n, v.bt, (uint64_t)v.B * v.max_blocks * 4);
+}
 
 // Enqueue the pack (dir = kPack) or unpack of the validated ranges.  The wire
 // is at `wire`; per (layer, K|V) slab it holds N*H*du units.
@@ -421,7 +435,8 @@ int stream_out(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1, const in
   if (need > dst_cap) return DV_ERR_SPACE;
   if (need == 0) return DV_OK;
   if (!dst || !aligned16(dst)) return DV_ERR_INVALID;
-  if (overlaps(dst, need, v.base, v.bytes)) return DV_ERR_INVALID;
+  if (overlaps(dst, need, v.base, v.bytes) || overlaps_table(v, dst, need))
+    return DV_ERR_INVALID;
   rc = check_kind_supported(v);
   if (rc != DV_OK) return rc;
   return run_stream(dv::kPack, v, l0, l1, r0, rn, N, dst, static_cast<hipStream_t>(stream));
@@ -592,9 +607,11 @@ int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const 
   if (src_bytes < need) return DV_ERR_SPACE;
   if (need == 0) return DV_OK;
   if (!src || !aligned16(src)) return DV_ERR_INVALID;
-  if (overlaps(src, need, v.base, v.bytes)) return DV_ERR_INVALID;
+  if (overlaps(src, need, v.base, v.bytes) || overlaps_table(v, v.base, v.bytes))
+    return DV_ERR_INVALID;
   if (v.owner && (overlaps(v.owner, (uint64_t)v.NB * 4, v.base, v.bytes) ||
-                  overlaps(v.owner, (uint64_t)v.NB * 4, src, need)))
+                  overlaps(v.owner, (uint64_t)v.NB * 4, src, need) ||
+                  overlaps_table(v, v.owner, (uint64_t)v.NB * 4)))
     return DV_ERR_INVALID;
   rc = check_kind_supported(v);
   if (rc != DV_OK) return rc;
@@ -613,7 +630,9 @@ int dv_block_claims(const dv_cache* c, int32_t mb, const int32_t* t0, const int3
   rc = ranges_of(v, 0, (int32_t)v.L, t0, t1, &r0, &rn, &N);
   if (rc != DV_OK) return rc;
   if (!counts || (reinterpret_cast<uintptr_t>(counts) & 3u) != 0) return DV_ERR_INVALID;
-  if (overlaps(counts, (uint64_t)v.NB * 4, v.base, v.bytes)) return DV_ERR_INVALID;
+  if (overlaps(counts, (uint64_t)v.NB * 4, v.base, v.bytes) ||
+      overlaps_table(v, counts, (uint64_t)v.NB * 4))
+    return DV_ERR_INVALID;
   hipStream_t st = static_cast<hipStream_t>(stream);
   for (int64_t g0 = 0; g0 < v.B; g0 += kSeqPerLaunch) {
     const int nseq = (int)std::min<int64_t>(kSeqPerLaunch, v.B - g0);

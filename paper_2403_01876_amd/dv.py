@@ -190,10 +190,11 @@ def _check(rc: int, name: str, check: bool):
     return rc
 
 
-def dv_cache_bytes(cache: Cache) -> int:
+def dv_cache_bytes(cache: Cache, check: bool = True):
     out = ctypes.c_uint64(0)
-    _check(lib.dv_cache_bytes(cache.ref, ctypes.byref(out)), "dv_cache_bytes", True)
-    return out.value
+    rc = lib.dv_cache_bytes(cache.ref, ctypes.byref(out))
+    _check(rc, "dv_cache_bytes", check)
+    return out.value if check else (rc, out.value)
 
 
 def dv_packed_bytes(cache: Cache, l0: int, l1: int, t0, t1, check: bool = True):

@@ -140,6 +140,42 @@ def test_owner_workspace_rejections():
     assert rc == dv.DV_ERR_INVALID
 
 
+def test_block_table_must_not_overlap_what_a_call_writes():
+    """The kernels read the block table while the call writes the stream's
+    destination (pack), the pool (unpack), the owner map or the claim
+    counts; a table overlapping any of them is refused on the host."""
+    L, H, D, B, NB, MB = 2, 4, 64, 3, 12, 4
+    pool = FAKE
+    pool_bytes = L * 2 * NB * H * 16 * D * 2
+    table_bytes = B * MB * 4
+    wire = FAKE + (1 << 34)
+    owner = FAKE + (1 << 36)
+    t1 = np.array([16, 33, 0], np.int32)
+
+    def paged(table, own=None):
+        return dv.Cache(dv.DV_PAGED, L, H, D, B, [pool], block_size=16, num_blocks=NB,
+                        max_blocks=MB, block_tables=[table], block_owners=[own])
+
+    need = dv.dv_packed_bytes(paged(FAKE + (1 << 35)), 0, L, None, t1)
+    bad = dv.DV_ERR_INVALID
+    # pack: the table inside the destination (its first or last bytes)
+    for table in (wire + need - 16, wire - table_bytes + 4):
+        rc, _ = dv.dv_stream_out_prompt(paged(table), 0, 0, L, None, t1, wire, need,
+                                        check=False)
+        assert rc == bad, hex(table)
+    # unpack: the table inside the pool, or inside the owner map
+    assert dv.dv_stream_in(paged(pool + pool_bytes - 8), 0, 0, L, None, t1, wire, need,
+                           check=False) == bad
+    assert dv.dv_stream_in(paged(owner + 16, owner), 0, 0, L, None, t1, wire, need,
+                           check=False) == bad
+    # claim counts over the table
+    counts = FAKE + (1 << 37)
+    assert dv.dv_block_claims(paged(counts + 4 * NB - 4), 0, None, t1, counts,
+                              check=False) == bad
+    # sizing does not look at addresses
+    assert dv.dv_packed_bytes(paged(pool), 0, L, None, t1) == need
+
+
 def test_range_errors():
     c = dense()
     z = np.zeros(4, np.int32)
@@ -394,6 +430,25 @@ def test_extent_limits_at_and_past_the_boundary():
     # capacity * head_dim * elem_bytes = 2^34 bytes
     assert sized(dense(L=1, H=1, D=512, B=1, S=1 << 24), 1) == (0, 2 * 1024)
     assert sized(dense(L=1, H=1, D=520, B=1, S=1 << 24), 1)[0] == U
+    # storage below 2^48 bytes: 2^13 layers x 2 x 2^10 sequences x 2^24 bytes
+    assert dv.dv_cache_bytes(dense(L=1 << 13, H=1, D=8, B=(1 << 10) - 1, S=1 << 20)) \
+        == (1 << 13) * 2 * ((1 << 10) - 1) * (1 << 24)
+    assert dv.dv_cache_bytes(dense(L=1 << 13, H=1, D=8, B=1 << 10, S=1 << 20), check=False)[0] == U
+    # a paged table can address more tokens than the pool holds: its longest
+    # stream (every sequence at capacity) is bounded the same way
+    def sized_b(c):
+        B = c.c.batch
+        return dv.dv_packed_bytes(c, 0, 1, np.zeros(B, np.int32), np.ones(B, np.int32),
+                                  check=False)
+
+    pg = lambda B: dv.Cache(dv.DV_PAGED, 1 << 13, 1, 8, B, [FAKE], block_size=16,  # noqa: E731
+                            num_blocks=4, max_blocks=1 << 16, block_tables=[FAKE])
+    assert sized_b(pg((1 << 10) - 1)) == (0, 2 * 16 * ((1 << 10) - 1))
+    assert sized_b(pg(1 << 10))[0] == U
+    # products that would wrap 64 bits are refused, not wrapped
+    assert sized(dense(L=1 << 30, H=1 << 4, D=128, B=1, S=1 << 24), 1)[0] == U
+    assert dv.dv_cache_bytes(dense(L=1 << 30, H=1 << 16, D=128, B=1 << 30, S=1 << 24),
+                             check=False)[0] == U
 
 
 def test_binding_refuses_range_arrays_shorter_than_the_batch():
