@@ -264,7 +264,9 @@ DV_API int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev
  * (measured on MI355X: with 4 queues and torch's stream pool the swap-in
  * and the step serialised; with 8 the swap-in hid behind the step).  Both
  * caches DV_DENSE with equal shapes (capacities may differ), dev in
- * DV_MEM_DEVICE, host in DV_MEM_HOST_PINNED.  One scheduler per host thread.
+ * DV_MEM_DEVICE, host in DV_MEM_HOST_PINNED; the two slots must be disjoint
+ * and so must the host mirrors (create returns DV_ERR_INVALID otherwise).
+ * One scheduler per host thread.
  * prefetch and end_step check their ranges against both the slots and the
  * host mirrors before enqueuing anything; a refused call changes nothing.
  * Errors: DV_ERR_INVALID (bad arguments; prefetch into a slot whose
@@ -301,8 +303,8 @@ DV_API int dv_swapper_destroy(dv_swapper* s);
  * layer ranges concatenate; decode steps can cycle through a few staging
  * slots while filling a long host log.
  * Pushes run in push order.  `staging` (device) and `dst` are caller owned,
- * disjoint from each other and from the source microbatch (create returns
- * DV_ERR_INVALID otherwise); offsets 16-byte aligned, each must hold its
+ * disjoint from each other, from the source microbatch and from a paged
+ * source's block table (create returns DV_ERR_INVALID otherwise); offsets 16-byte aligned, each must hold its
  * offset + bytes (else DV_ERR_SPACE).  create allocates
  * one stream, 64 events and the worker thread; push blocks only when 64
  * pushes are waiting for the worker.  flush blocks until everything pushed

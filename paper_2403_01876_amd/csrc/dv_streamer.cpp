@@ -170,6 +170,15 @@ int dv_streamer_create(const dv_cache* src, int32_t mb, void* staging, uint64_t 
       overlaps(dst, dst_cap, src->mb_base[mb], bytes) ||
       overlaps(staging, staging_cap, dst, dst_cap))
     return DV_ERR_INVALID;
+  // A paged source's block table is read by every pack: neither the staging
+  // nor the destination may cover it.
+  if (src->kind == DV_PAGED) {
+    const void* table = src->block_table[mb];
+    const uint64_t table_bytes = (uint64_t)src->batch * src->max_blocks * 4;
+    if (overlaps(staging, staging_cap, table, table_bytes) ||
+        overlaps(dst, dst_cap, table, table_bytes))
+      return DV_ERR_INVALID;
+  }
   dv_streamer* s = new (std::nothrow) dv_streamer();
   if (!s) return DV_ERR_INVALID;
   s->src = *src;

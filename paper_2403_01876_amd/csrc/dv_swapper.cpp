@@ -11,7 +11,9 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "../../include/dv.h"
@@ -56,6 +58,22 @@ int check_ranges(const dv_swapper* s, const int32_t* t0, const int32_t* t1) {
   return rc;
 }
 
+// Whether the n regions [base[i], base[i] + bytes) are non-null, 16-byte
+// aligned and pairwise disjoint.
+bool disjoint_regions(void* const* base, int64_t n, uint64_t bytes) {
+  std::vector<uintptr_t> a;
+  a.reserve(n);
+  for (int64_t i = 0; i < n; ++i) {
+    const uintptr_t p = reinterpret_cast<uintptr_t>(base[i]);
+    if (p == 0 || (p & 15u) != 0) return false;
+    a.push_back(p);
+  }
+  std::sort(a.begin(), a.end());
+  for (size_t i = 1; i < a.size(); ++i)
+    if (a[i] - a[i - 1] < bytes) return false;
+  return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -69,11 +87,17 @@ int dv_swapper_create(const dv_cache* dev_slots, const dv_cache* host, dv_swappe
       dev_slots->head_dim != host->head_dim || dev_slots->batch != host->batch ||
       dev_slots->elem_bytes != host->elem_bytes)
     return DV_ERR_INVALID;
-  uint64_t bytes = 0;
-  int rc = dv_cache_bytes(dev_slots, &bytes);
+  uint64_t slot_bytes = 0, host_bytes = 0;
+  int rc = dv_cache_bytes(dev_slots, &slot_bytes);
   if (rc != DV_OK) return rc;
-  rc = dv_cache_bytes(host, &bytes);
+  rc = dv_cache_bytes(host, &host_bytes);
   if (rc != DV_OK) return rc;
+  // A prefetch writes one slot while the step reads the other, and swaps
+  // move between mirrors and slots concurrently: the two slots must be
+  // disjoint, and so must the host mirrors.
+  if (!disjoint_regions(dev_slots->mb_base, 2, slot_bytes) ||
+      !disjoint_regions(host->mb_base, host->num_mb, host_bytes))
+    return DV_ERR_INVALID;
   dv_swapper* s = new (std::nothrow) dv_swapper();
   if (!s) return DV_ERR_INVALID;
   // Own copies of the base arrays: the caller's may go away after this call.

@@ -282,6 +282,17 @@ def test_swapper_create_rejections():
                      max_blocks=4, block_tables=[FAKE, FAKE])
     assert dv.lib.dv_swapper_create(paged.ref, host.ref, C.byref(h)) == dv.DV_ERR_UNSUPPORTED
     assert dv.lib.dv_swapper_create(dev.ref, host.ref, None) == dv.DV_ERR_INVALID
+    # the two slots must be disjoint, and so must the host mirrors (which
+    # hold 2*2*4*3*64*64*2 bytes each here)
+    mirror = 2 * 2 * 4 * 3 * 64 * 64 * 2
+    mirrors = [FAKE + (1 << 34) + i * mirror for i in range(4)]
+    apart = dense(bases=mirrors, mem=dv.DV_MEM_HOST_PINNED, S=64)
+    for slots in ((FAKE, FAKE), (FAKE, FAKE + 2 * 2 * 4 * 3 * 50 * 64 * 2 - 16), (FAKE, 0)):
+        assert dv.lib.dv_swapper_create(dense(bases=slots).ref, apart.ref, C.byref(h)) == \
+            dv.DV_ERR_INVALID, slots
+    for bases in (mirrors[:3] + [mirrors[1] + 16], mirrors[:3] + [mirrors[3] + 8]):
+        hosts = dense(bases=bases, mem=dv.DV_MEM_HOST_PINNED, S=64)
+        assert dv.lib.dv_swapper_create(dev.ref, hosts.ref, C.byref(h)) == dv.DV_ERR_INVALID
     assert h.value is None
     for f in ("dv_swapper_sync", "dv_swapper_destroy"):
         assert getattr(dv.lib, f)(None) == dv.DV_ERR_INVALID
@@ -310,7 +321,13 @@ def test_streamer_create_rejections():
                                      C.byref(h)) == dv.DV_ERR_INVALID
     assert dv.lib.dv_streamer_create(c.ref, 0, st, 1 << 20, FAKE + 4096, 1 << 20,
                                      C.byref(h)) == dv.DV_ERR_INVALID
-    assert h.value is None
+    # nor may staging or destination cover a paged source's block table
+    table = FAKE + (1 << 35)
+    pg = dv.Cache(dv.DV_PAGED, 2, 4, 64, 3, [FAKE], block_size=16, num_blocks=12,
+                  max_blocks=4, block_tables=[table])
+    for stg, dst in ((table - 64, other), (st, table + 40)):
+        assert dv.lib.dv_streamer_create(pg.ref, 0, stg, 1 << 10, dst, 1 << 10,
+                                         C.byref(h)) == dv.DV_ERR_INVALID, (hex(stg), hex(dst))
     assert h.value is None
     for f in ("dv_streamer_flush", "dv_streamer_destroy"):
         assert getattr(dv.lib, f)(None) == dv.DV_ERR_INVALID
