@@ -216,11 +216,30 @@ def main_step_bench(args, torch, dv, synth):
         b.record(stream)
         torch.cuda.synchronize()
         kern[name] = a.elapsed_time(b) / args.steps
+    # The copy ceiling: a plain contiguous copy of the same P bytes, timed the
+    # same way, in the pack kernel's launch shape (the layout is the only
+    # difference left).
+    from paper_2403_01876_amd import baseline
+
+    def plain(s):
+        baseline.plain_copy(wire, sender, P, s)
+
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    plain(stream)
+    a.record(stream)
+    for _ in range(args.steps):
+        plain(stream)
+    b.record(stream)
+    torch.cuda.synchronize()
+    kern["plain_copy"] = a.elapsed_time(b) / args.steps
+    checks["plain_copy_equals_source"] = bool(torch.equal(wire[:P], sender[:P]))
     step_bytes = 2 * P * 2 + w.steps * 2 * I * 2
     res = {
         "ms": ms, "eager_ms": eager_ms, "graph_ms": graph_ms, "P": P, "I": I,
         "step_bytes": step_bytes, "value": step_bytes / (ms * 1e-3) / 1e9,
-        "pack_ms": kern["pack"], "unpack_ms": kern["unpack"], "checks": checks,
+        "pack_ms": kern["pack"], "unpack_ms": kern["unpack"], "copy_ms": kern["plain_copy"],
+        "checks": checks,
     }
     del sender, recv, wire, incs, graph
     torch.cuda.empty_cache()
@@ -1172,6 +1191,7 @@ def main():
     w, r = main_step_bench(args, torch, dv, synth)
     pack_gbs = 2 * r["P"] / (r["pack_ms"] * 1e-3) / 1e9
     unpack_gbs = 2 * r["P"] / (r["unpack_ms"] * 1e-3) / 1e9
+    copy_gbs = 2 * r["P"] / (r["copy_ms"] * 1e-3) / 1e9
     out = {
         "metric": METRIC,
         "value": round(r["value"], 2),
@@ -1209,6 +1229,14 @@ def main():
             "traffic": counted_traffic(),
             "avg_ms": round(r["pack_ms"], 4),
             "bytes_per_launch": 2 * r["P"],
+            "copy_ceiling": {
+                "what": "plain contiguous 16-byte copy of the same P bytes in the pack "
+                        "kernel's launch shape (libdv_baseline dvb_plain_copy)",
+                "avg_ms": round(r["copy_ms"], 4),
+                "GBps": round(copy_gbs, 1),
+                "frac": round(copy_gbs / HBM_PEAK_GBS, 4),
+                "kernel_vs_copy": round(pack_gbs / copy_gbs, 4),
+            },
         },
         "kernels": {
             "dense_runs_kernel<unpack>": {"avg_ms": round(r["unpack_ms"], 4),

@@ -1,7 +1,9 @@
-"""ctypes binding of the per-region copy baseline (``libdv_baseline.so``).
+"""ctypes binding of the comparison baselines (``libdv_baseline.so``).
 
-One copy call per contiguous region (the comparison baseline of the paper's
-evaluation, Sec. 5.1); used by the benchmark and its parity test only.
+``per_region_copy``: one copy call per contiguous region (the comparison
+baseline of the paper's evaluation, Sec. 5.1).  ``plain_copy``: a contiguous
+16-byte copy with the pack kernel's launch shape, the ceiling the streaming
+kernels are set against.  Used by the benchmark and its tests only.
 """
 from __future__ import annotations
 
@@ -26,6 +28,8 @@ def _load():
         lib.dvb_per_region_copy.argtypes = [ctypes.POINTER(dv.dv_cache), i32, i32, i32, vp, vp,
                                             vp, ctypes.c_uint64, vp]
         lib.dvb_per_region_copy.restype = ctypes.c_int64
+        lib.dvb_plain_copy.argtypes = [vp, vp, ctypes.c_uint64, vp]
+        lib.dvb_plain_copy.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -40,3 +44,9 @@ def per_region_copy(cache: dv.Cache, mb: int, l0: int, l1: int, t0, t1, dst, dst
     if n < 0:
         raise dv.DvError(int(n), "dvb_per_region_copy")
     return int(n)
+
+
+def plain_copy(dst, src, nbytes: int, stream=None) -> None:
+    rc = _load().dvb_plain_copy(dv._addr(dst), dv._addr(src), nbytes, dv._stream(stream))
+    if rc != dv.DV_OK:
+        raise dv.DvError(int(rc), "dvb_plain_copy")

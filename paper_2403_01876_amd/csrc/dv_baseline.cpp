@@ -1,15 +1,84 @@
-// Comparison baseline of the paper's evaluation (Sec. 5.1, "Baseline"): the
-// non-contiguous cache region is moved with one copy call per contiguous
-// region instead of being packed into a temporary buffer first.  It is not
-// part of the streaming path; the benchmark times it against the buffered
-// path (pack kernel + one copy), and the tests check it produces the same
-// bytes in the same order.
+// Comparison baselines, not part of the streaming path.
+//
+// dvb_per_region_copy is the baseline of the paper's evaluation (Sec. 5.1,
+// "Baseline"): the non-contiguous cache region is moved with one copy call
+// per contiguous region instead of being packed into a temporary buffer
+// first.  The benchmark times it against the buffered path (pack kernel +
+// one copy), and the tests check it produces the same bytes in the same
+// order.
+//
+// dvb_plain_copy is the copy ceiling the pack and unpack kernels are set
+// against: a contiguous 16-byte copy with their per-lane shape (two
+// nontemporal units per lane, loads before stores, 256 lanes per workgroup)
+// and their XCD dealing, so the only difference left is the cache layout.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "../../include/dv.h"
 
+namespace {
+
+constexpr int kCopyThreads = 256;
+constexpr int kCopyUnroll = 2;
+constexpr uint32_t kXcds = 8;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// The hardware deals workgroups to the 8 XCDs in turn.  Workgroup b is
+// renumbered so that XCD b % 8 copies one contiguous share of the tiles:
+// XCD x owns the (tiles + 7 - x) / 8 workgroups with b % 8 == x, placed after
+// the shares of XCDs 0 .. x-1.  A bijection on [0, tiles).
+__device__ uint32_t xcd_tile(uint32_t b, uint32_t tiles) {
+  const uint32_t x = b % kXcds, i = b / kXcds;
+  uint32_t start = 0;
+  for (uint32_t y = 0; y < x; ++y) start += (tiles + kXcds - 1 - y) / kXcds;
+  return start + i;
+}
+
+__global__ void __launch_bounds__(kCopyThreads)
+    plain_copy_kernel(const u32x4* src, u32x4* dst, uint64_t units, uint32_t tiles) {
+  const uint64_t u0 = (uint64_t)xcd_tile(blockIdx.x, tiles) * (kCopyThreads * kCopyUnroll) +
+                      threadIdx.x;
+  u32x4 v[kCopyUnroll];
+#pragma unroll
+  for (int k = 0; k < kCopyUnroll; ++k) {
+    uint64_t u = u0 + (uint64_t)k * kCopyThreads;
+    if (u >= units) u = units - 1;  // clamped: every load issues before any store
+    v[k] = __builtin_nontemporal_load(src + u);
+  }
+#pragma unroll
+  for (int k = 0; k < kCopyUnroll; ++k) {
+    const uint64_t u = u0 + (uint64_t)k * kCopyThreads;
+    if (u < units) __builtin_nontemporal_store(v[k], dst + u);
+  }
+}
+
+}  // namespace
+
 extern "C" {
+
+// Copies `bytes` (a multiple of 16; both addresses 16-byte aligned, the
+// regions disjoint) from `src` to `dst` on `stream`.  DV_OK, DV_ERR_INVALID,
+// DV_ERR_UNSUPPORTED (2^31 or more tiles of 8 KB), DV_ERR_HIP.
+DV_API int dvb_plain_copy(void* dst, const void* src, uint64_t bytes, void* stream) {
+  const uintptr_t d = reinterpret_cast<uintptr_t>(dst), s = reinterpret_cast<uintptr_t>(src);
+  if (!dst || !src || (d & 15u) || (s & 15u) || (bytes & 15u)) return DV_ERR_INVALID;
+  if (d < s + bytes && s < d + bytes && bytes) return DV_ERR_INVALID;
+  if (bytes == 0) return DV_OK;
+  const uint64_t units = bytes / 16;
+  const uint64_t tiles = (units + kCopyThreads * kCopyUnroll - 1) / (kCopyThreads * kCopyUnroll);
+  if (tiles >= (1ull << 31)) return DV_ERR_UNSUPPORTED;
+  const u32x4* from = static_cast<const u32x4*>(src);
+  u32x4* to = static_cast<u32x4*>(dst);
+  uint64_t n = units;
+  uint32_t t = (uint32_t)tiles;
+  void* args[] = {&from, &to, &n, &t};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&plain_copy_kernel), dim3(t),
+                         dim3(kCopyThreads), args, 0, static_cast<hipStream_t>(stream)) ==
+                 hipSuccess
+             ? DV_OK
+             : DV_ERR_HIP;
+}
 
 // Dense caches only: for each (layer, K|V, sequence, head) of the ranges,
 // one hipMemcpyAsync of the run of tokens [t0[b], t1[b]) into `dst` at its

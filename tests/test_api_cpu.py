@@ -333,6 +333,20 @@ def test_streamer_create_rejections():
         assert getattr(dv.lib, f)(None) == dv.DV_ERR_INVALID
 
 
+def test_plain_copy_baseline_rejections():
+    """The copy-ceiling baseline checks its arguments before launching."""
+    from paper_2403_01876_amd import baseline
+    lib = baseline._load()
+    bad = dv.DV_ERR_INVALID
+    for dst, src, n in ((FAKE + 8, FAKE + (1 << 30), 64),      # misaligned destination
+                        (FAKE, FAKE + (1 << 30) + 4, 64),      # misaligned source
+                        (FAKE, FAKE + (1 << 30), 60),          # not whole 16-byte units
+                        (FAKE, FAKE + 32, 64),                 # overlapping regions
+                        (None, FAKE, 64)):
+        assert lib.dvb_plain_copy(dst, src, n, None) == bad, (dst, src, n)
+    assert lib.dvb_plain_copy(FAKE, FAKE + 16, 0, None) == dv.DV_OK  # nothing to copy
+
+
 def test_binding_fails_loudly_without_the_library(tmp_path):
     """No fallback: a copy of the package without libdv.so refuses to import."""
     import shutil

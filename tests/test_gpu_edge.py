@@ -350,6 +350,22 @@ def test_per_region_baseline_matches_buffered(oracle_lib, seed):
     assert h_buf.numpy()[:n].tobytes() == exp.tobytes()
 
 
+@pytest.mark.parametrize("units", [1, 255, 512, 513, 8 * 512 + 7, 5 * 8 * 512 + 300])
+def test_plain_copy_baseline(units):
+    """The copy ceiling the benchmark sets the pack kernel against copies
+    exactly its bytes: sizes below one 8 KB tile, at and past tile edges, and
+    tile counts that do not divide by the 8 XCDs (the workgroup renumbering
+    must stay a bijection); the bytes past the end stay untouched."""
+    from paper_2403_01876_amd import baseline
+    n = units * 16
+    src = G.to_dev(synth.fill_bytes(n, units))
+    dst = G.dev_const(n + 64, 0x5C)
+    baseline.plain_copy(dst, src, n, stream())
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:n], src)
+    assert bool((dst[n:] == 0x5C).all())
+
+
 def test_binding_follows_torchs_current_stream(oracle_lib):
     """stream=None means torch's current stream: under torch.cuda.stream(s)
     the pack runs after the work already queued on s (here a long spin and
