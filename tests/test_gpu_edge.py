@@ -323,6 +323,64 @@ def test_graph_replay_matches_eager(oracle_lib):
     del eager_recv
 
 
+@pytest.mark.parametrize("kind", ["dense", "paged"])
+def test_graph_replay_short_runs(oracle_lib, kind):
+    """Multi-token steps (3 tokens per sequence, the short-run kernel)
+    captured once and replayed four times, with eager work and syncs in
+    between: every replay leaves each step's wire and the receiver equal to
+    the oracle's."""
+    r = np.random.default_rng(11)
+    L, H, D, B, K, steps = 2, 4, 64, 5, 3, 5
+    if kind == "dense":
+        S = 64
+        lay = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S)
+        extents = dict(max_seq=S)
+        kd = dv.DV_DENSE
+    else:
+        bs, maxb = 16, 4
+        bt, nb = synth.make_paged_tables(9, [maxb * bs] * B, bs, maxb)
+        lay = oracle.Layout(oracle.PAGED, L, H, D, B, block_size=bs, num_blocks=nb,
+                            block_table=bt)
+        extents = dict(block_size=bs, num_blocks=nb, max_blocks=maxb,
+                       block_tables=[G.to_dev(bt)])
+        kd = dv.DV_PAGED
+    host = synth.fill_bytes(lay.storage_bytes(), 13)
+    cs = dv.Cache(kd, L, H, D, B, [G.to_dev(host)], **extents)
+    recv = G.dev_const(lay.storage_bytes(), 0)
+    cr = dv.Cache(kd, L, H, D, B, [recv], **extents)
+    p0 = r.integers(0, 40, size=B).astype(np.int32)
+    rng = [(p0 + K * i, p0 + K * (i + 1)) for i in range(steps)]
+    n = dv.dv_packed_bytes(cs, 0, L, *rng[0])
+    wires = [G.dev_const(n, 0) for _ in range(steps)]
+
+    def step(st):
+        for (a, e), wb in zip(rng, wires):
+            dv.dv_stream_out_prompt(cs, 0, 0, L, a, e, wb, n, st)
+            dv.dv_stream_in(cr, 0, 0, L, a, e, wb, n, st)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            step(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    exp_wires = [oracle_lib.pack(lay, host, 0, L, a, e) for a, e in rng]
+    for rep in range(4):
+        recv.fill_(rep + 7)
+        for wb in wires:
+            wb.fill_(0x33)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        exp = np.full(lay.storage_bytes(), rep + 7, np.uint8)
+        for (a, e), ew in zip(rng, exp_wires):
+            oracle_lib.unpack(lay, exp, 0, L, a, e, ew)
+        for wb, ew in zip(wires, exp_wires):
+            assert G.host(wb).tobytes() == ew.tobytes(), rep
+        assert G.host(recv).tobytes() == exp.tobytes(), rep
+
+
 @pytest.mark.parametrize("seed", range(4))
 def test_per_region_baseline_matches_buffered(oracle_lib, seed):
     """The comparison baseline (one copy per contiguous region) yields the same
