@@ -310,9 +310,10 @@ DV_API int dv_swapper_destroy(dv_swapper* s);
  * pushes are waiting for the worker.  flush blocks until everything pushed
  * has reached `dst` and returns the first error the worker met (a later
  * push also returns it).  destroy drains, then frees.  Same alignment,
- * range and layout rules as dv_stream_out_prompt.  push is not for a stream
- * under graph capture: the worker waits on the host for the event it
- * records, which a capture never completes. */
+ * range and layout rules as dv_stream_out_prompt.  push refuses a compute
+ * stream under graph capture (DV_ERR_INVALID, nothing recorded): the worker
+ * waits on the host for the event push records, which a capture would only
+ * turn into a graph node. */
 typedef struct dv_streamer dv_streamer;
 DV_API int dv_streamer_create(const dv_cache* src, int32_t mb, void* staging, uint64_t staging_cap,
                        void* dst, uint64_t dst_cap, dv_streamer** out);

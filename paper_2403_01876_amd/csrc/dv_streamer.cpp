@@ -233,6 +233,12 @@ int dv_streamer_push(dv_streamer* s, void* compute_stream, int32_t l0, int32_t l
   if (staging_offset > s->staging_cap || bytes > s->staging_cap - staging_offset ||
       dst_offset > s->dst_cap || bytes > s->dst_cap - dst_offset)
     return DV_ERR_SPACE;
+  // The worker waits on the host for the event recorded below; under graph
+  // capture that record is only a graph node, so the push is refused.
+  hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(static_cast<hipStream_t>(compute_stream), &capture) != hipSuccess)
+    return DV_ERR_HIP;
+  if (capture != hipStreamCaptureStatusNone) return DV_ERR_INVALID;
   Request r;
   r.l0 = l0;
   r.l1 = l1;

@@ -156,5 +156,26 @@ def test_streamer_errors_surface():
     assert rc == dv.DV_ERR_INVALID  # unaligned offset
     rc, n = s.push(0, 1, [0, 0], [1, 1], 0, 4096, check=False)
     assert rc == dv.DV_ERR_SPACE  # destination offset past the end
+    # a compute stream under graph capture is refused and the capture goes on
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            cache.add_(1)
+            rc, n = s.push(0, 1, [0, 0], [1, 1], 0, stream=torch.cuda.current_stream(),
+                           check=False)
+            cache.add_(1)
+    assert rc == dv.DV_ERR_INVALID
+    g.replay()
+    torch.cuda.synchronize()
+    assert int(cache[0]) == 2  # the capture holds both adds
     assert s.flush() == dv.DV_OK
+    # after the refusals the streamer still works
+    assert s.push(0, 1, [0, 0], [1, 1], 0) == 2 * 2 * 64 * 2
+    assert s.flush() == dv.DV_OK
+    torch.cuda.synchronize()
+    exp = torch.cat([cache[0:128], cache[16 * 128:17 * 128], cache[2 * 16 * 128:2 * 16 * 128 + 128],
+                     cache[3 * 16 * 128:3 * 16 * 128 + 128]])
+    assert torch.equal(dst[:512], exp)
     s.close()
