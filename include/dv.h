@@ -269,6 +269,9 @@ DV_API int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev
  * One scheduler per host thread.
  * prefetch and end_step check their ranges against both the slots and the
  * host mirrors before enqueuing anything; a refused call changes nothing.
+ * begin_step and end_step refuse a compute stream under graph capture
+ * (DV_ERR_INVALID): the scheduler's streams wait on events the caller's
+ * stream records, which a capture would only turn into graph nodes.
  * Errors: DV_ERR_INVALID (bad arguments; prefetch into a slot whose
  * occupant's step has not ended), DV_ERR_RANGE (microbatch outside `host`;
  * begin/end of a microbatch not prefetched; ranges that do not fit),

@@ -74,6 +74,16 @@ bool disjoint_regions(void* const* base, int64_t n, uint64_t bytes) {
   return true;
 }
 
+// The scheduler orders its streams against the caller's with events; a
+// compute stream under graph capture would turn those into graph nodes the
+// scheduler's own streams cannot wait for, so such calls are refused.
+int refuse_capture(void* stream, int* rc) {
+  hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(static_cast<hipStream_t>(stream), &capture) != hipSuccess)
+    return *rc = DV_ERR_HIP;
+  return *rc = capture == hipStreamCaptureStatusNone ? DV_OK : DV_ERR_INVALID;
+}
+
 }  // namespace
 
 extern "C" {
@@ -167,6 +177,8 @@ int dv_swapper_begin_step(dv_swapper* s, int32_t mb, void* compute_stream, int32
   if (mb < 0 || mb >= s->host.num_mb) return DV_ERR_RANGE;
   const int slot = s->slot_of[mb];
   if (slot < 0) return DV_ERR_RANGE;  // not prefetched
+  int rc = DV_OK;
+  if (refuse_capture(compute_stream, &rc) != DV_OK) return rc;
   if (hipStreamWaitEvent(static_cast<hipStream_t>(compute_stream), s->resident[slot], 0) !=
       hipSuccess)
     return DV_ERR_HIP;
@@ -182,6 +194,7 @@ int dv_swapper_end_step(dv_swapper* s, int32_t mb, void* compute_stream, const i
   if (slot < 0) return DV_ERR_RANGE;
   int rc = check_ranges(s, t0, t1);
   if (rc != DV_OK) return rc;
+  if (refuse_capture(compute_stream, &rc) != DV_OK) return rc;
   rc = hip_ok(hipEventRecord(s->step_done, static_cast<hipStream_t>(compute_stream)));
   if (rc != DV_OK) return rc;
   if (hipStreamWaitEvent(s->s_out, s->step_done, 0) != hipSuccess) return DV_ERR_HIP;

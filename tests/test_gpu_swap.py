@@ -305,6 +305,23 @@ def test_swapper_refuses_refill_before_step_end():
     assert sw.prefetch(2, lens, check=False) == dv.DV_ERR_INVALID
     with pytest.raises(dv.DvError):
         sw.begin_step(2)  # not prefetched
+    # begin_step and end_step refuse a stream under graph capture, and the
+    # capture goes on
+    scratch = G.dev_const(64, 0)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            scratch.add_(1)
+            cap = torch.cuda.current_stream()
+            with pytest.raises(dv.DvError) as e:
+                sw.begin_step(0, stream=cap)
+            assert e.value.status == dv.DV_ERR_INVALID
+            assert sw.end_step(0, [3], [4], stream=cap, check=False) == dv.DV_ERR_INVALID
+    g.replay()
+    torch.cuda.synchronize()
+    assert int(scratch[0]) == 1
     assert sw.begin_step(0) == 0
     sw.end_step(0, [3], [4])
     assert sw.prefetch(2, lens) == dv.DV_OK  # slot 0 is free again
