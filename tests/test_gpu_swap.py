@@ -146,6 +146,54 @@ def test_swap_engines_match_oracle(oracle_lib, case):
     assert G.host(slot2).tobytes() == exp_slot.tobytes()
 
 
+@pytest.mark.parametrize("engine", ["kernel", "dma"])
+def test_swaps_replay_from_a_graph(oracle_lib, engine):
+    """Swap-out then swap-in captured once and replayed three times, with the
+    slot and the mirror rewritten between replays: narrow rows (one-token
+    updates, the copy kernel) and whole prompts (2-D copies on the DMA
+    engines).  Every replay moves the oracle's bytes."""
+    L, H, D, B, S = 2, 3, 64, 4, 96
+    dl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S)
+    if engine == "kernel":
+        t0 = np.array([5, 17, 0, 40], np.int32)
+        t1 = t0 + 1
+    else:  # the DMA engines take rows of 64 KB or more: 1 KB tokens, runs of 64-77
+        D, S = 512, 80
+        dl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S)
+        t0 = np.array([0, 3, 0, 10], np.int32)
+        t1 = np.array([70, 80, 64, 75], np.int32)
+    slot = G.dev_const(dl.storage_bytes(), 0)
+    back = G.dev_const(dl.storage_bytes(), 0)
+    host = pinned(dl.storage_bytes(), 0)
+    d = dv.Cache(dv.DV_DENSE, L, H, D, B, [slot], max_seq=S)
+    d2 = dv.Cache(dv.DV_DENSE, L, H, D, B, [back], max_seq=S)
+    h = dv.Cache(dv.DV_DENSE, L, H, D, B, [host.data_ptr()], max_seq=S,
+                 mem=dv.DV_MEM_HOST_PINNED)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            cur = torch.cuda.current_stream()
+            dv.dv_swap_out(d, 0, h, 0, 0, L, t0, t1, cur)
+            dv.dv_swap_in(h, 0, d2, 0, 0, L, t0, t1, cur)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        slot_h = synth.fill_bytes(dl.storage_bytes(), 70 + rep)
+        slot.copy_(torch.from_numpy(slot_h))
+        host.fill_(0x40 + rep)
+        back.fill_(0x90 + rep)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        exp_host = np.full(dl.storage_bytes(), 0x40 + rep, np.uint8)
+        oracle_lib.copy_ranges(dl, slot_h, dl, exp_host, 0, L, t0, t1)
+        assert host.numpy().tobytes() == exp_host.tobytes(), rep
+        exp_back = np.full(dl.storage_bytes(), 0x90 + rep, np.uint8)
+        oracle_lib.copy_ranges(dl, exp_host, dl, exp_back, 0, L, t0, t1)
+        assert G.host(back).tobytes() == exp_back.tobytes(), rep
+
+
 def test_opt66b_round_robin_swapping(oracle_lib):
     """Four microbatches through two device slots, two rounds.
 
