@@ -205,17 +205,19 @@ def main_step_bench(args, torch, dv, synth):
     # Per-kernel durations: one event pair around back-to-back launches that
     # follow a leading untimed one, so the queue never drains and the mean is
     # pure kernel time (an event pair per launch would add its own packets).
+    # Single launches vary by about 1 %, so at least 20 are averaged.
     kern = {}
+    nk = max(args.steps, 20)
     for name, fn in (("pack", pack), ("unpack", unpack)):
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
         fn(stream)
         a.record(stream)
-        for _ in range(args.steps):
+        for _ in range(nk):
             fn(stream)
         b.record(stream)
         torch.cuda.synchronize()
-        kern[name] = a.elapsed_time(b) / args.steps
+        kern[name] = a.elapsed_time(b) / nk
     # The copy ceiling: a plain contiguous copy of the same P bytes, timed the
     # same way, in the pack kernel's launch shape (the layout is the only
     # difference left).
@@ -228,11 +230,11 @@ def main_step_bench(args, torch, dv, synth):
     b = torch.cuda.Event(enable_timing=True)
     plain(stream)
     a.record(stream)
-    for _ in range(args.steps):
+    for _ in range(nk):
         plain(stream)
     b.record(stream)
     torch.cuda.synchronize()
-    kern["plain_copy"] = a.elapsed_time(b) / args.steps
+    kern["plain_copy"] = a.elapsed_time(b) / nk
     checks["plain_copy_equals_source"] = bool(torch.equal(wire[:P], sender[:P]))
     step_bytes = 2 * P * 2 + w.steps * 2 * I * 2
     res = {
