@@ -256,13 +256,20 @@ DV_API int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev
  *                                      on the scheduler's output stream.
  * Slots are dealt alternately in prefetch order.  Ordering is by HIP events
  * only; no call blocks the host except dv_swapper_sync and destroy.
- * create allocates two streams and five events (the only allocations);
+ * create allocates four streams and five events (the only allocations);
  * the descriptors' base arrays are copied.  Overlap needs the scheduler's
- * streams on hardware queues of their own: HIP maps streams onto
- * GPU_MAX_HW_QUEUES hardware queues (4 by default) and streams sharing a
- * queue execute in order, so a process with many streams should raise it
- * (measured on MI355X: with 4 queues and torch's stream pool the swap-in
- * and the step serialised; with 8 the swap-in hid behind the step).  Both
+ * streams on hardware queues other than the compute stream's: HIP deals
+ * ordinary streams onto a pool of GPU_MAX_HW_QUEUES hardware queues (4 by
+ * default) and streams sharing a queue execute in order.  The input and the
+ * output stream therefore each come in two forms: one with a hardware queue
+ * of its own (a CU-masked stream over every CU, which HIP never shares), used
+ * when the compute stream of the latest begin_step / end_step is not the
+ * legacy null stream, and one from the shared pool, used otherwise (HIP
+ * makes CU-masked streams wait for the null stream).  With the null stream
+ * as compute stream a process with many streams should raise
+ * GPU_MAX_HW_QUEUES, or compute on a stream of its own (measured on MI355X:
+ * a pooled stream landed on the compute stream's queue in one creation of
+ * four; the own-queue form never did).  Both
  * caches DV_DENSE with equal shapes (capacities may differ), dev in
  * DV_MEM_DEVICE, host in DV_MEM_HOST_PINNED; the two slots must be disjoint
  * and so must the host mirrors (create returns DV_ERR_INVALID otherwise).
@@ -307,9 +314,12 @@ DV_API int dv_swapper_destroy(dv_swapper* s);
  * slots while filling a long host log.
  * Pushes run in push order.  `staging` (device) and `dst` are caller owned,
  * disjoint from each other, from the source microbatch and from a paged
- * source's block table (create returns DV_ERR_INVALID otherwise); offsets 16-byte aligned, each must hold its
- * offset + bytes (else DV_ERR_SPACE).  create allocates
- * one stream, 64 events and the worker thread; push blocks only when 64
+ * source's block table (create returns DV_ERR_INVALID otherwise); offsets
+ * 16-byte aligned, each must hold its offset + bytes (else DV_ERR_SPACE).
+ * create allocates two side streams (one with a hardware queue of its own,
+ * used for pushes from any compute stream but the legacy null stream, and
+ * one from HIP's shared pool for pushes from the null stream; see the swap
+ * scheduler), 64 events and the worker thread; push blocks only when 64
  * pushes are waiting for the worker.  flush blocks until everything pushed
  * has reached `dst` and returns the first error the worker met (a later
  * push also returns it).  destroy drains, then frees.  Same alignment,

@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "../../include/dv.h"
+#include "dv_host.h"
 #include "dv_internal.h"
 
 namespace {
@@ -537,6 +538,23 @@ int swap_copy(const dv_cache* from, int32_t from_mb, const dv_cache* to, int32_t
 }
 
 }  // namespace
+
+namespace dv {
+
+hipError_t create_side_streams(hipStream_t* shared_queue, hipStream_t* own_queue) {
+  *shared_queue = *own_queue = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(shared_queue, hipStreamNonBlocking);
+  if (e != hipSuccess) return e;
+  int device = 0, cus = 0;
+  e = hipGetDevice(&device);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
+  if (e != hipSuccess || cus <= 0) return e != hipSuccess ? e : hipErrorInvalidDevice;
+  std::vector<uint32_t> mask((cus + 31) / 32, 0xffffffffu);  // every CU
+  if (cus % 32) mask.back() = (1u << (cus % 32)) - 1u;
+  return hipExtStreamCreateWithCUMask(own_queue, (uint32_t)mask.size(), mask.data());
+}
+
+}  // namespace dv
 
 extern "C" {
 

@@ -7,7 +7,9 @@
 // an event on the compute stream and hands a request to the worker thread;
 // the worker waits for that event on the host, then, on the streamer's side
 // stream, packs the region into device staging (the buffered copy of
-// optimisation 1) and copies the staged chunk to its destination.  The compute thread pays one event
+// optimisation 1) and copies the staged chunk to its destination.  The side
+// stream has a hardware queue of its own unless the compute stream is the
+// legacy null stream.  The compute thread pays one event
 // record and a queue push per region; the GPU overlaps the streaming with
 // whatever the compute stream runs next.
 //
@@ -27,6 +29,7 @@
 #include <vector>
 
 #include "../../include/dv.h"
+#include "dv_host.h"
 
 namespace {
 
@@ -40,6 +43,7 @@ struct Request {
   std::vector<int32_t> t0, t1;
   uint64_t staging_off, dst_off, bytes;
   int event;  // index into the pool
+  hipStream_t side;  // the side stream form for the pushing compute stream
 };
 
 }  // namespace
@@ -55,7 +59,10 @@ struct dv_streamer {
   uint64_t dst_cap = 0;
   bool dst_host = false;  // destination in host memory: pitched (SDMA) copies
   int device = 0;
-  hipStream_t side = nullptr;
+  // The side stream in two forms (see create_side_streams): [0] on HIP's
+  // shared hardware queues, for a compute stream that is the legacy null
+  // stream; [1] on a hardware queue of its own, for any other.
+  hipStream_t side[2] = {};
   hipEvent_t events[kEventPool] = {};
   std::vector<int> free_events;
   std::deque<Request> queue;
@@ -69,17 +76,17 @@ struct dv_streamer {
 
 namespace {
 
-hipError_t copy_out(dv_streamer* s, char* dst, const char* src, uint64_t n) {
-  if (!s->dst_host) return hipMemcpyAsync(dst, src, n, hipMemcpyDefault, s->side);
+hipError_t copy_out(dv_streamer* s, hipStream_t side, char* dst, const char* src, uint64_t n) {
+  if (!s->dst_host) return hipMemcpyAsync(dst, src, n, hipMemcpyDefault, side);
   const uint64_t rows = n / kHostRow, tail = n - rows * kHostRow;
   if (rows) {
     const hipError_t e = hipMemcpy2DAsync(dst, kHostRow, src, kHostRow, kHostRow, rows,
-                                          hipMemcpyDeviceToHost, s->side);
+                                          hipMemcpyDeviceToHost, side);
     if (e != hipSuccess) return e;
   }
   if (tail)
     return hipMemcpy2DAsync(dst + rows * kHostRow, tail, src + rows * kHostRow, tail, tail, 1,
-                            hipMemcpyDeviceToHost, s->side);
+                            hipMemcpyDeviceToHost, side);
   return hipSuccess;
 }
 
@@ -112,11 +119,12 @@ void run_worker(dv_streamer* s) {
     s->cv.notify_all();
     if (rc == DV_OK && r.bytes > 0) {
       rc = dv_stream_out_prompt(&s->src, s->mb, r.l0, r.l1, r.t0.data(), r.t1.data(),
-                                s->staging + r.staging_off, r.bytes, nullptr, s->side);
+                                s->staging + r.staging_off, r.bytes, nullptr, r.side);
       if (rc == DV_OK &&
-          copy_out(s, s->dst + r.dst_off, s->staging + r.staging_off, r.bytes) != hipSuccess)
+          copy_out(s, r.side, s->dst + r.dst_off, s->staging + r.staging_off, r.bytes) !=
+              hipSuccess)
         rc = DV_ERR_HIP;
-      if (rc == DV_OK && hipStreamSynchronize(s->side) != hipSuccess) rc = DV_ERR_HIP;
+      if (rc == DV_OK && hipStreamSynchronize(r.side) != hipSuccess) rc = DV_ERR_HIP;
     }
     {
       std::lock_guard<std::mutex> lk(s->m);
@@ -136,10 +144,12 @@ void release(dv_streamer* s) {
     s->cv.notify_all();
     s->worker.join();
   }
-  if (s->side) (void)hipStreamSynchronize(s->side);
+  for (hipStream_t x : s->side)
+    if (x) (void)hipStreamSynchronize(x);
   for (hipEvent_t e : s->events)
     if (e) (void)hipEventDestroy(e);
-  if (s->side) (void)hipStreamDestroy(s->side);
+  for (hipStream_t x : s->side)
+    if (x) (void)hipStreamDestroy(x);
   delete s;
 }
 
@@ -204,7 +214,7 @@ int dv_streamer_create(const dv_cache* src, int32_t mb, void* staging, uint64_t 
     s->dst_host = true;
   }
   if (hipGetDevice(&s->device) != hipSuccess ||
-      hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking) != hipSuccess) {
+      dv::create_side_streams(&s->side[0], &s->side[1]) != hipSuccess) {
     release(s);
     return DV_ERR_HIP;
   }
@@ -249,6 +259,7 @@ int dv_streamer_push(dv_streamer* s, void* compute_stream, int32_t l0, int32_t l
   r.staging_off = staging_offset;
   r.dst_off = dst_offset;
   r.bytes = bytes;
+  r.side = dv::pick_side(compute_stream, s->side[0], s->side[1]);
   {
     std::unique_lock<std::mutex> lk(s->m);
     if (s->error != DV_OK) return s->error;
@@ -276,7 +287,8 @@ int dv_streamer_flush(dv_streamer* s) {
     std::unique_lock<std::mutex> lk(s->m);
     s->cv.wait(lk, [s] { return s->queue.empty() && s->busy == 0; });
   }
-  if (hipStreamSynchronize(s->side) != hipSuccess) return DV_ERR_HIP;
+  for (hipStream_t x : s->side)
+    if (hipStreamSynchronize(x) != hipSuccess) return DV_ERR_HIP;
   std::lock_guard<std::mutex> lk(s->m);
   return s->error;
 }

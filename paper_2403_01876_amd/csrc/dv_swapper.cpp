@@ -17,11 +17,17 @@
 #include <vector>
 
 #include "../../include/dv.h"
+#include "dv_host.h"
 
 struct dv_swapper {
   dv_cache dev, host;
   std::vector<void*> dev_base, host_base;
-  hipStream_t s_in = nullptr, s_out = nullptr;
+  // Input and output streams, each in two forms (see create_side_streams):
+  // [0] on HIP's shared hardware queues, [1] on a hardware queue of its own.
+  // own_queue picks between them: the form for the compute stream of the
+  // latest begin_step / end_step (shared queues until one has been seen).
+  hipStream_t s_in[2] = {}, s_out[2] = {};
+  bool own_queue = false;
   hipEvent_t resident[2] = {nullptr, nullptr};  // swap-in into the slot done
   hipEvent_t freed[2] = {nullptr, nullptr};     // slot's last occupant swapped out
   hipEvent_t step_done = nullptr;
@@ -38,15 +44,19 @@ namespace {
 int hip_ok(hipError_t e) { return e == hipSuccess ? DV_OK : DV_ERR_HIP; }
 
 void release(dv_swapper* s) {
-  if (s->s_in) (void)hipStreamSynchronize(s->s_in);
-  if (s->s_out) (void)hipStreamSynchronize(s->s_out);
+  for (int i = 0; i < 2; ++i) {
+    if (s->s_in[i]) (void)hipStreamSynchronize(s->s_in[i]);
+    if (s->s_out[i]) (void)hipStreamSynchronize(s->s_out[i]);
+  }
   for (int i = 0; i < 2; ++i) {
     if (s->resident[i]) (void)hipEventDestroy(s->resident[i]);
     if (s->freed[i]) (void)hipEventDestroy(s->freed[i]);
   }
   if (s->step_done) (void)hipEventDestroy(s->step_done);
-  if (s->s_in) (void)hipStreamDestroy(s->s_in);
-  if (s->s_out) (void)hipStreamDestroy(s->s_out);
+  for (int i = 0; i < 2; ++i) {
+    if (s->s_in[i]) (void)hipStreamDestroy(s->s_in[i]);
+    if (s->s_out[i]) (void)hipStreamDestroy(s->s_out[i]);
+  }
   delete s;
 }
 
@@ -122,8 +132,8 @@ int dv_swapper_create(const dv_cache* dev_slots, const dv_cache* host, dv_swappe
   s->dev.block_owner = s->host.block_owner = nullptr;
   s->slot_of.assign(host->num_mb, -1);
   // Streams at the default priority.
-  if (hipStreamCreateWithFlags(&s->s_in, hipStreamNonBlocking) != hipSuccess ||
-      hipStreamCreateWithFlags(&s->s_out, hipStreamNonBlocking) != hipSuccess) {
+  if (dv::create_side_streams(&s->s_in[0], &s->s_in[1]) != hipSuccess ||
+      dv::create_side_streams(&s->s_out[0], &s->s_out[1]) != hipSuccess) {
     release(s);
     return DV_ERR_HIP;
   }
@@ -158,11 +168,11 @@ int dv_swapper_prefetch(dv_swapper* s, int32_t mb, const int32_t* len) {
   int rc = check_ranges(s, nullptr, len);
   if (rc != DV_OK) return rc;
   // The slot is reused only after its previous occupant's update has left.
-  if (prev >= 0 && hipStreamWaitEvent(s->s_in, s->freed[slot], 0) != hipSuccess)
-    return DV_ERR_HIP;
-  rc = dv_swap_in(&s->host, mb, &s->dev, slot, 0, s->host.num_layers, nullptr, len, s->s_in);
+  const hipStream_t in = s->s_in[s->own_queue ? 1 : 0];
+  if (prev >= 0 && hipStreamWaitEvent(in, s->freed[slot], 0) != hipSuccess) return DV_ERR_HIP;
+  rc = dv_swap_in(&s->host, mb, &s->dev, slot, 0, s->host.num_layers, nullptr, len, in);
   if (rc != DV_OK) return rc;
-  rc = hip_ok(hipEventRecord(s->resident[slot], s->s_in));
+  rc = hip_ok(hipEventRecord(s->resident[slot], in));
   if (rc != DV_OK) return rc;
   if (prev >= 0) s->slot_of[prev] = -1;
   s->occupant[slot] = mb;
@@ -182,6 +192,7 @@ int dv_swapper_begin_step(dv_swapper* s, int32_t mb, void* compute_stream, int32
   if (hipStreamWaitEvent(static_cast<hipStream_t>(compute_stream), s->resident[slot], 0) !=
       hipSuccess)
     return DV_ERR_HIP;
+  s->own_queue = dv::pick_side(compute_stream, s->s_in[0], s->s_in[1]) == s->s_in[1];
   *slot_out = slot;
   return DV_OK;
 }
@@ -197,18 +208,22 @@ int dv_swapper_end_step(dv_swapper* s, int32_t mb, void* compute_stream, const i
   if (refuse_capture(compute_stream, &rc) != DV_OK) return rc;
   rc = hip_ok(hipEventRecord(s->step_done, static_cast<hipStream_t>(compute_stream)));
   if (rc != DV_OK) return rc;
-  if (hipStreamWaitEvent(s->s_out, s->step_done, 0) != hipSuccess) return DV_ERR_HIP;
-  rc = dv_swap_out(&s->dev, slot, &s->host, mb, 0, s->host.num_layers, t0, t1, s->s_out);
+  const hipStream_t out = dv::pick_side(compute_stream, s->s_out[0], s->s_out[1]);
+  s->own_queue = out == s->s_out[1];
+  if (hipStreamWaitEvent(out, s->step_done, 0) != hipSuccess) return DV_ERR_HIP;
+  rc = dv_swap_out(&s->dev, slot, &s->host, mb, 0, s->host.num_layers, t0, t1, out);
   if (rc != DV_OK) return rc;
-  rc = hip_ok(hipEventRecord(s->freed[slot], s->s_out));
+  rc = hip_ok(hipEventRecord(s->freed[slot], out));
   if (rc == DV_OK) s->done[slot] = true;
   return rc;
 }
 
 int dv_swapper_sync(dv_swapper* s) {
   if (!s) return DV_ERR_INVALID;
-  if (hipStreamSynchronize(s->s_in) != hipSuccess) return DV_ERR_HIP;
-  if (hipStreamSynchronize(s->s_out) != hipSuccess) return DV_ERR_HIP;
+  for (int i = 0; i < 2; ++i)
+    if (hipStreamSynchronize(s->s_in[i]) != hipSuccess ||
+        hipStreamSynchronize(s->s_out[i]) != hipSuccess)
+      return DV_ERR_HIP;
   return DV_OK;
 }
 

@@ -285,10 +285,14 @@ def test_opt66b_round_robin_swapping(oracle_lib):
         G.assert_dense_ranges_equal(slots[0], refs[x], L, B, H, S, D, E, 0, L, zero, lens[x])
 
 
-def test_swapper_round_robin(oracle_lib):
+@pytest.mark.parametrize("compute_kind", ["null", "own", "alternating"])
+def test_swapper_round_robin(oracle_lib, compute_kind):
     """The scheduler runs the protocol of the previous test by itself: five
     microbatches (an odd count, so slots alternate differently each round)
-    through two slots, three rounds, ragged per-sequence positions."""
+    through two slots, three rounds, ragged per-sequence positions.  The
+    compute stream is the legacy null stream (pooled side streams), a stream
+    of its own (side streams on hardware queues of their own), or the two in
+    turn, step by step (the scheduler switching forms mid-protocol)."""
     L, H, D, B, E = 3, 4, 128, 3, 2
     S, S_host, M = 64, 48, 5
     dl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S, elem_bytes=E)
@@ -302,7 +306,10 @@ def test_swapper_round_robin(oracle_lib):
                   mem=dv.DV_MEM_HOST_PINNED)
     zero = np.zeros(B, np.int32)
     lens = [np.array([20, 25, 30], np.int32) + x for x in range(M)]
-    compute = torch.cuda.current_stream()
+    null = torch.cuda.default_stream()
+    own = torch.cuda.Stream()
+    own.wait_stream(torch.cuda.current_stream())
+    compute = null
     for x in range(M):
         dv.dv_swap_out(dr, x, hh, x, 0, L, zero, lens[x], compute)
     compute.synchronize()
@@ -315,6 +322,7 @@ def test_swapper_round_robin(oracle_lib):
     sched = list(swap_model.swap_schedule(M, 3))
     sw.prefetch(sched[0][0], lens[sched[0][0]])
     for k, (x, xn, _) in enumerate(sched):
+        compute = {"null": null, "own": own}.get(compute_kind, null if k % 2 == 0 else own)
         if xn is not None:
             sw.prefetch(xn, lens[xn])
         slot = sw.begin_step(x, compute)
