@@ -307,7 +307,10 @@ DV_API int dv_swapper_destroy(dv_swapper* s);
  * copies the packed bytes to `dst` + dst_offset (pinned host memory, or
  * device memory; a host destination is written by pitched copies, which run
  * on the SDMA engines and leave the compute units to the compute stream,
- * where a plain copy would run as a blit kernel on them).  Offsets are the
+ * where a plain copy would run as a blit kernel on them).  From a DV_DENSE
+ * source whose longest (sequence, head) run in the region is 64 KB or more,
+ * a host destination is filled by the SDMA engines straight from the cache
+ * (pitched copies over the heads' runs, no kernel and no staging).  Offsets are the
  * caller's: pushing a prompt's layers one by one at offsets that accumulate
  * their sizes leaves the whole prompt's contiguous buffer in `dst`, since
  * layer ranges concatenate; decode steps can cycle through a few staging

@@ -21,6 +21,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <condition_variable>
 #include <deque>
 #include <mutex>
@@ -37,6 +38,12 @@ constexpr int kEventPool = 64;
 // Row width of the pitched host copies: whole rows go as one copy, the
 // remainder as a one-row copy.
 constexpr uint64_t kHostRow = 256u << 10;
+// A dense source whose longest (sequence, head) run is at least this long
+// goes to a host destination by the DMA engines directly, as the swaps do:
+// one pitched copy per (layer, K|V, sequence) over the heads' runs, or one
+// for the whole region when every sequence has the same range.  No pack
+// kernel then shares the compute units with the compute stream.
+constexpr uint64_t kDmaRunBytes = 64u << 10;
 
 struct Request {
   int32_t l0, l1;
@@ -90,6 +97,54 @@ hipError_t copy_out(dv_streamer* s, hipStream_t side, char* dst, const char* src
   return hipSuccess;
 }
 
+// Whether request r goes by the DMA engines straight from the cache.
+bool dma_direct(const dv_streamer* s, const Request& r) {
+  if (!s->dst_host || s->src.kind != DV_DENSE) return false;
+  const uint64_t tok = (uint64_t)s->src.head_dim * s->src.elem_bytes;
+  int32_t longest = 0;
+  for (int32_t b = 0; b < s->src.batch; ++b) longest = std::max(longest, r.t1[b] - r.t0[b]);
+  return (uint64_t)longest * tok >= kDmaRunBytes;
+}
+
+// The region of request r, in the contiguous buffer's order, from the dense
+// cache to dst + r.dst_off: row (slab, sequence b, head h) holds b's run of
+// h, at pitch max_seq * tok in the cache and n_b * tok in the buffer.
+hipError_t dma_gather(dv_streamer* s, const Request& r, hipStream_t side) {
+  const dv_cache& c = s->src;
+  const uint64_t tok = (uint64_t)c.head_dim * c.elem_bytes, B = c.batch, H = c.num_heads;
+  const uint64_t row = (uint64_t)c.max_seq * tok;  // cache pitch of one (slab, b, h) run
+  const char* cache = static_cast<const char*>(c.mb_base[s->mb]);
+  char* out = s->dst + r.dst_off;
+  uint64_t N = 0;
+  bool uniform = true;
+  for (uint64_t b = 0; b < B; ++b) {
+    N += (uint64_t)(r.t1[b] - r.t0[b]);
+    if (r.t0[b] != r.t0[0] || r.t1[b] != r.t1[0]) uniform = false;
+  }
+  if (uniform) {  // rows (slab, b, h) follow each other at one pitch on both sides
+    const uint64_t n = (uint64_t)(r.t1[0] - r.t0[0]);
+    if (n == 0) return hipSuccess;
+    return hipMemcpy2DAsync(out, n * tok, cache + 2 * r.l0 * B * H * row + r.t0[0] * tok, row,
+                            n * tok, 2 * (uint64_t)(r.l1 - r.l0) * B * H, hipMemcpyDeviceToHost,
+                            side);
+  }
+  for (uint64_t slab = 2 * r.l0; slab < 2 * (uint64_t)r.l1; ++slab) {
+    uint64_t p = 0;  // tokens of earlier sequences
+    for (uint64_t b = 0; b < B; ++b) {
+      const uint64_t n = (uint64_t)(r.t1[b] - r.t0[b]);
+      if (n > 0) {
+        const hipError_t e = hipMemcpy2DAsync(
+            out + ((slab - 2 * r.l0) * N + p) * H * tok, n * tok,
+            cache + (slab * B + b) * H * row + r.t0[b] * tok, row, n * tok, H,
+            hipMemcpyDeviceToHost, side);
+        if (e != hipSuccess) return e;
+      }
+      p += n;
+    }
+  }
+  return hipSuccess;
+}
+
 void run_worker(dv_streamer* s) {
   (void)hipSetDevice(s->device);
   for (;;) {
@@ -118,12 +173,16 @@ void run_worker(dv_streamer* s) {
     }
     s->cv.notify_all();
     if (rc == DV_OK && r.bytes > 0) {
-      rc = dv_stream_out_prompt(&s->src, s->mb, r.l0, r.l1, r.t0.data(), r.t1.data(),
-                                s->staging + r.staging_off, r.bytes, nullptr, r.side);
-      if (rc == DV_OK &&
-          copy_out(s, r.side, s->dst + r.dst_off, s->staging + r.staging_off, r.bytes) !=
-              hipSuccess)
-        rc = DV_ERR_HIP;
+      if (dma_direct(s, r)) {
+        if (dma_gather(s, r, r.side) != hipSuccess) rc = DV_ERR_HIP;
+      } else {
+        rc = dv_stream_out_prompt(&s->src, s->mb, r.l0, r.l1, r.t0.data(), r.t1.data(),
+                                  s->staging + r.staging_off, r.bytes, nullptr, r.side);
+        if (rc == DV_OK &&
+            copy_out(s, r.side, s->dst + r.dst_off, s->staging + r.staging_off, r.bytes) !=
+                hipSuccess)
+          rc = DV_ERR_HIP;
+      }
       if (rc == DV_OK && hipStreamSynchronize(r.side) != hipSuccess) rc = DV_ERR_HIP;
     }
     {

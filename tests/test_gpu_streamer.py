@@ -16,23 +16,31 @@ from paper_2403_01876_amd import dv  # noqa: E402
 from tests import gpu_util as G  # noqa: E402
 
 
-def test_layer_by_layer_prompt_to_host(oracle_lib):
+@pytest.mark.parametrize("case", ["ragged", "uniform", "short"])
+def test_layer_by_layer_prompt_to_host(oracle_lib, case):
     """Each layer is written by the compute stream just before it is pushed;
-    the host buffer ends up holding the whole prompt's contiguous buffer."""
+    the host buffer ends up holding the whole prompt's contiguous buffer.
+    Runs of 64 KB or more go by the DMA engines straight from the cache (one
+    pitched copy per layer slab and sequence, or one per layer when every
+    sequence has the same range); shorter ones through the pack kernel and
+    the staging buffer."""
     L, H, D, B, S = 6, 3, 128, 4, 300
     lay = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S)
     cache = G.dev_const(lay.storage_bytes(), 0xA5)  # not yet computed
     c = dv.Cache(dv.DV_DENSE, L, H, D, B, [cache], max_seq=S)
-    lens = np.array([300, 17, 0, 129], np.int32)
+    lens = {"ragged": np.array([300, 17, 0, 129], np.int32),
+            "uniform": np.full(B, 280, np.int32),
+            "short": np.array([100, 17, 0, 129], np.int32)}[case]
     zero = np.zeros(B, np.int32)
     total = dv.dv_packed_bytes(c, 0, L, zero, lens)
     staging = G.dev_const(total, 0)
     host = torch.full((total,), 0x11, dtype=torch.uint8, pin_memory=True)
     layer_wires = [synth.fill_bytes(dv.dv_packed_bytes(c, l, l + 1, zero, lens), 10 + l)
                    for l in range(L)]
-    # a host destination is written in 256 KiB rows plus a remainder: each
-    # layer here is two whole rows and a tail
-    assert all(w.size // (256 << 10) == 2 and w.size % (256 << 10) for w in layer_wires)
+    if case == "ragged":
+        # through staging a host destination is written in 256 KiB rows plus
+        # a remainder; these layers would be two whole rows and a tail
+        assert all(w.size // (256 << 10) == 2 and w.size % (256 << 10) for w in layer_wires)
     dev_wires = [G.to_dev(wl) for wl in layer_wires]
     torch.cuda.synchronize()
     compute = torch.cuda.Stream()
