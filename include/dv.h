@@ -254,9 +254,16 @@ DV_API int dv_swap_in(const dv_cache* host, int32_t host_mb, const dv_cache* dev
  *                                      out the part the step updated (tokens
  *                                      [t0[b], t1[b]), e.g. the one new token)
  *                                      on the scheduler's output stream.
- * Slots are dealt alternately in prefetch order.  Ordering is by HIP events
- * only; no call blocks the host except dv_swapper_sync and destroy.
- * create allocates four streams and five events (the only allocations);
+ * Slots are dealt alternately in prefetch order.  The calls keep the slot
+ * bookkeeping and hand each swap to a worker thread, which waits on the host
+ * for what the swap depends on (the step, before a swap-out; the slot's
+ * previous swap-out, before a swap-in) and then issues it, so that only the
+ * compute stream waits on the GPU, for residency (streams waiting on the GPU
+ * behind a swap-in stretched it by about 0.46 ms each on MI355X).
+ * begin_step blocks the host until the worker has issued that microbatch's
+ * swap-in; end_step blocks only if 8 swap-outs are still waiting for their
+ * steps.  create allocates four streams, twelve events and the worker thread
+ * (the only allocations);
  * the descriptors' base arrays are copied.  Overlap needs the scheduler's
  * streams on hardware queues other than the compute stream's: HIP deals
  * ordinary streams onto a pool of GPU_MAX_HW_QUEUES hardware queues (4 by
