@@ -352,6 +352,73 @@ static void case_swap(hipStream_t st, const int32_t* t0, const int32_t* t1, cons
   HIPCHECK(hipHostFree(mirror));
 }
 
+/* The swap scheduler: three host microbatches through two slots for two
+   rounds; each step writes one token per sequence into its slot, and the
+   scheduler swaps that update out.  Every mirror then equals the oracle's. */
+static void case_scheduler(hipStream_t st) {
+  enum { L = 2, H = 3, D = 64, B = 3, S = 64, M = 3, ROUNDS = 2 };
+  dvo_layout od = dense_oracle(DV_DENSE, L, H, D, B, S);
+  const size_t bytes = (size_t)dvo_storage_elems(&od) * 2;
+  void* slots[2];
+  void* mirrors[M];
+  uint8_t* exp[M];
+  int32_t len[M][B];
+  for (int i = 0; i < 2; ++i) {
+    HIPCHECK(hipMalloc(&slots[i], bytes));
+    HIPCHECK(hipMemset(slots[i], 0, bytes));
+  }
+  for (int x = 0; x < M; ++x) {
+    exp[x] = host_filled(bytes, 200 + x);
+    HIPCHECK(hipHostMalloc(&mirrors[x], bytes, hipHostMallocDefault));
+    memcpy(mirrors[x], exp[x], bytes);
+    for (int b = 0; b < B; ++b) len[x][b] = 20 + 3 * b + x;
+  }
+  dv_cache dev = dense_desc(DV_DENSE, L, H, D, B, S, DV_MEM_DEVICE, slots);
+  dev.num_mb = 2;
+  dv_cache hst = dense_desc(DV_DENSE, L, H, D, B, S, DV_MEM_HOST_PINNED, mirrors);
+  hst.num_mb = M;
+  dv_swapper* sw = NULL;
+  EXPECT(dv_swapper_create(&dev, &hst, &sw) == DV_OK, "dv_swapper_create");
+  const int32_t one[B] = {1, 1, 1};
+  uint64_t n = 0;
+  {
+    int32_t t1[B];
+    for (int b = 0; b < B; ++b) t1[b] = one[b];
+    EXPECT(dv_packed_bytes(&dev, 0, L, NULL, t1, &n) == DV_OK, "token size");
+  }
+  void* wire = NULL;
+  HIPCHECK(hipMalloc(&wire, n));
+  EXPECT(dv_swapper_prefetch(sw, 0, len[0]) == DV_OK, "first prefetch");
+  for (int k = 0; k < ROUNDS * M; ++k) {
+    const int x = k % M, xn = (k + 1) % M;
+    if (k + 1 < ROUNDS * M)
+      EXPECT(dv_swapper_prefetch(sw, xn, len[xn]) == DV_OK, "prefetch");
+    int32_t slot = -1;
+    EXPECT(dv_swapper_begin_step(sw, x, st, &slot) == DV_OK, "begin_step");
+    int32_t t1[B];
+    for (int b = 0; b < B; ++b) t1[b] = len[x][b] + 1;
+    uint8_t* tok = host_filled(n, 700 + k);
+    HIPCHECK(hipMemcpyAsync(wire, tok, n, hipMemcpyHostToDevice, st));
+    EXPECT(dv_stream_in(&dev, slot, 0, L, len[x], t1, wire, n, st) == DV_OK, "step's token");
+    EXPECT(dvo_unpack(&od, exp[x], 0, L, len[x], t1, tok) == DVO_OK, "oracle token");
+    EXPECT(dv_swapper_end_step(sw, x, st, len[x], t1) == DV_OK, "end_step");
+    HIPCHECK(hipStreamSynchronize(st));  /* the token's host buffer is reused */
+    free(tok);
+    for (int b = 0; b < B; ++b) len[x][b] += 1;
+  }
+  EXPECT(dv_swapper_sync(sw) == DV_OK, "dv_swapper_sync");
+  EXPECT(dv_swapper_destroy(sw) == DV_OK, "dv_swapper_destroy");
+  for (int x = 0; x < M; ++x) same(mirrors[x], exp[x], bytes, "scheduler mirror against the oracle");
+  printf("swap scheduler: %d microbatches, %d rounds through 2 slots, bit-exact\n", M, ROUNDS);
+  ++cases;
+  for (int x = 0; x < M; ++x) {
+    free(exp[x]);
+    HIPCHECK(hipHostFree(mirrors[x]));
+  }
+  for (int i = 0; i < 2; ++i) HIPCHECK(hipFree(slots[i]));
+  HIPCHECK(hipFree(wire));
+}
+
 int main(void) {
   int ndev = 0;
   HIPCHECK(hipGetDeviceCount(&ndev));
@@ -389,6 +456,7 @@ int main(void) {
     const int32_t t1[4] = {512, 300, 520, 0};
     case_swap(st, t0, t1, "swap of long rows (DMA engine)");
   }
+  case_scheduler(st);
   HIPCHECK(hipStreamDestroy(st));
   printf("abi parity ok: %d cases\n", cases);
   return 0;

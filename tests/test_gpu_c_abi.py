@@ -33,4 +33,4 @@ def test_c_program_streams_bit_exact():
     r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     print(r.stdout, r.stderr, flush=True)
     assert r.returncode == 0, r.stdout + r.stderr
-    assert "abi parity ok: 6 cases" in r.stdout
+    assert "abi parity ok: 7 cases" in r.stdout
