@@ -1265,6 +1265,7 @@ def main():
             "dense_runs_kernel<unpack>": {"avg_ms": round(r["unpack_ms"], 4),
                                           "GBps_2x": round(unpack_gbs, 1),
                                           "frac_hbm": round(unpack_gbs / HBM_PEAK_GBS, 4),
+                                          "kernel_vs_copy": round(unpack_gbs / copy_gbs, 4),
                                           "traffic": counted_traffic(
                                               "traffic_bytes_per_launch_unpack")},
         },
