@@ -17,10 +17,13 @@ headline).  ``value`` is algorithmic bytes per step (every payload byte read
 once and written once: 2 x payload per call) over the step time, in GB/s.
 ``roofline`` is the bulk pack kernel (the dense-run kernel of the prompt
 stream-out), its duration from HIP events around back-to-back launches on its
-stream.  Further objects report the other kernels, the microbatch swap over
-the host link (OPT-66B stage), the paged gather/scatter (LLaMA-2-70B GQA),
-the full-cache replica and restore (BLOOM-176B shard), and the oracle timed
-on the host cores.
+stream, with a plain copy of the same bytes beside it (``copy_ceiling``).
+Further objects report the other kernels, the microbatch swap over the host
+link and the swap scheduler's protocol (OPT-66B stage), the paged
+gather/scatter (LLaMA-2-70B GQA), the full-cache replica and restore
+(BLOOM-176B shard), multi-token steps, streaming overlapped with emulated
+compute, ring recovery, buffered against per-region copies, and the oracle
+timed on the host cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--eager]
                        [--extras all|bulk|calib|swap|none] [--no-cpu-baseline]
