@@ -68,8 +68,10 @@ typedef enum {
                               capacity (max_seq, or max_blocks*block_size) above 2^24,
                               head_dim*elem_bytes above 2^20 bytes, num_heads*head_dim*
                               elem_bytes above 2^24 bytes, capacity*head_dim*elem_bytes above
-                              2^34 bytes, a cache whose storage, or whose stream of every
-                              layer and sequence at full capacity, reaches 2^48 bytes,
+                              2^34 bytes, a paged block of one head (block_size*head_dim*
+                              elem_bytes) above 2^33 bytes, a cache whose storage, or
+                              whose stream of every layer and sequence at full capacity,
+                              reaches 2^48 bytes,
                               or a launch whose grid would count 2^31 or more
                               tiles or 16-byte units (each launch covers up to 64
                               sequences; every launch of a call is checked first) */

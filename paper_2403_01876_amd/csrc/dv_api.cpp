@@ -86,6 +86,9 @@ int layout_of(const dv_cache* c, View* v) {
   if (v->cap > (1 << 24) || v->du > (1 << 16) || v->H * v->du > (1 << 20) ||
       v->cap * v->du > (1ll << 30))
     return DV_ERR_UNSUPPORTED;
+  // The paged kernel flattens (head pair, unit) over two heads of one block:
+  // 2 * block_size * du units must stay well inside int32.
+  if (c->kind == DV_PAGED && v->bs * v->du > (1ll << 29)) return DV_ERR_UNSUPPORTED;
   // Every byte count derived from the descriptor stays far inside 64 bits:
   // its storage and the longest stream it can produce (all layers, every
   // sequence at full capacity) must be below 2^48 bytes.

@@ -452,6 +452,14 @@ def test_extent_limits_at_and_past_the_boundary():
                                   num_blocks=4, max_blocks=maxb, block_tables=[FAKE])
     assert sized(paged(1 << 20), 1 << 24) == (0, 2 * 16 << 24)
     assert sized(paged((1 << 20) + 1), 1)[0] == U
+    # one head of a paged block: block_size * head_dim * elem_bytes = 2^33
+    # bytes (2^29 units; the paged kernel counts two heads' units in int32)
+    # (within the capacity limits above only for head_dim * elem_bytes >= 2^9)
+    blk = lambda bs: dv.Cache(dv.DV_PAGED, 1, 1, 512, 1, [FAKE], block_size=bs,  # noqa: E731
+                              num_blocks=4, max_blocks=1, block_tables=[FAKE])
+    assert sized(blk(1 << 23), 1) == (0, 2 * 1024)
+    assert sized(blk((1 << 23) + 1), 1)[0] == U
+    assert dv.dv_cache_bytes(blk((1 << 23) + 1), check=False)[0] == U
     # head_dim * elem_bytes = 2^20 bytes (2^16 units)
     assert sized(dense(L=1, H=1, D=1 << 19, B=1, S=2), 1) == (0, 2 << 20)
     assert sized(dense(L=1, H=1, D=(1 << 19) + 8, B=1, S=2), 1)[0] == U

@@ -1,6 +1,6 @@
 """The largest extents the library accepts, on the GPU.
 
-* a dense cache of 34 GiB, so cache addresses pass 2**31 16-byte units;
+* a dense cache of 68 GiB, so cache addresses pass 2**32 16-byte units;
 * the 2**24-token capacity with capacity * head_dim * elem_bytes at its
   2**34-byte limit (32 GiB), for a prompt range and a decode-step token at
   the last position;

@@ -1,4 +1,6 @@
 """Microbatch swapping between device slots and pinned host mirrors."""
+import zlib
+
 import numpy as np
 import pytest
 
@@ -103,7 +105,8 @@ def test_swap_engines_match_oracle(oracle_lib, case):
     """Both engines: narrow rows (copy kernel) and rows of 64 KB or more (DMA)."""
     L, H, D, B, E = 2, 3, 128, 5, 2
     S_dev, S_host = 600, 520
-    r = np.random.default_rng(hash(case) % 1000)
+    # a fixed seed per case (str hashes change from process to process)
+    r = np.random.default_rng(zlib.crc32(case.encode()))
     if case == "delta-uniform":
         t0 = np.full(B, 300, np.int32)
         t1 = t0 + 1
