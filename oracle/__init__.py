@@ -135,6 +135,24 @@ class Oracle:
         assert rc == OK
         return wire
 
+    def pack_into(self, lay: Layout, cache: np.ndarray, l0, l1, t0, t1,
+                  out: np.ndarray) -> None:
+        """As ``pack``, into the first wire bytes of the contiguous uint8
+        array ``out``."""
+        cache = np.ascontiguousarray(cache)
+        assert cache.nbytes >= lay.storage_bytes()
+        assert out.dtype == np.uint8 and out.flags.c_contiguous
+        a0, p0 = self._r(t0)
+        a1, p1 = self._r(t1)
+        rc = self.lib.dvo_check(ctypes.byref(lay._c), l0, l1, p0, p1)
+        if rc != OK:
+            raise ValueError(f"oracle rejects ranges ({rc})")
+        n = self.lib.dvo_wire_elems(ctypes.byref(lay._c), l0, l1, p0, p1)
+        assert out.nbytes >= n * lay.elem_bytes
+        rc = self.lib.dvo_pack(ctypes.byref(lay._c), cache.ctypes.data, l0, l1, p0, p1,
+                               out.ctypes.data)
+        assert rc == OK
+
     def unpack(self, lay: Layout, cache: np.ndarray, l0, l1, t0, t1, wire: np.ndarray) -> None:
         """Writes the ranges of ``cache`` (in place) from ``wire``."""
         assert cache.flags.c_contiguous and cache.nbytes >= lay.storage_bytes()

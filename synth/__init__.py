@@ -107,6 +107,43 @@ def fill_bytes(nbytes: int, seed: int, first_byte: int = 0) -> np.ndarray:
     return fill_bytes_numpy(nbytes, seed, first_byte)
 
 
+def host_threads() -> int:
+    """Host threads for the parallel helpers: the process's CPU affinity."""
+    try:
+        return max(1, len(os.sched_getaffinity(0)))
+    except AttributeError:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def fill_into(out: np.ndarray, seed: int, first_byte: int = 0,
+              threads: Optional[int] = None) -> np.ndarray:
+    """Fill the contiguous uint8 array ``out`` with stream bytes
+    ``first_byte .. first_byte + out.size``, split into chunks filled on
+    ``threads`` host threads (the C twin releases the GIL)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    assert out.dtype == np.uint8 and out.flags.c_contiguous
+    lib = _host_lib()
+    n = out.size
+    if lib is None:
+        out[:] = fill_bytes_numpy(n, seed, first_byte)
+        return out
+    chunk = 1 << 26
+    base = out.ctypes.data
+
+    def one(off):
+        lib.dvsynth_host_fill(base + off, min(chunk, n - off), seed & MASK64, first_byte + off)
+
+    with ThreadPoolExecutor(threads or host_threads()) as ex:
+        list(ex.map(one, range(0, n, chunk)))
+    return out
+
+
+def fill_bytes_parallel(nbytes: int, seed: int, threads: Optional[int] = None) -> np.ndarray:
+    """``fill_bytes(nbytes, seed)`` on several host threads."""
+    return fill_into(np.empty(nbytes, dtype=np.uint8), seed, 0, threads)
+
+
 def fill_bytes_numpy(nbytes: int, seed: int, first_byte: int = 0) -> np.ndarray:
     """The numpy statement of the same definition (reference for the C twin)."""
     w0 = first_byte // 8

@@ -31,6 +31,27 @@ def dev_const(nbytes: int, byte: int) -> torch.Tensor:
     return torch.full((max(nbytes, 16),), byte, dtype=torch.uint8, device=DEV)
 
 
+def assert_same_bytes(dev: torch.Tensor, exp: np.ndarray, what: str,
+                      chunk: int = 1 << 30) -> int:
+    """Every byte of the host array ``exp`` equals the byte at the same offset
+    of the device buffer ``dev`` (compared on the device, ``chunk`` bytes at
+    a time).  Returns the number of bytes compared."""
+    e8 = np.ascontiguousarray(exp).view(np.uint8).reshape(-1)
+    d8 = dev.view(torch.uint8).reshape(-1)
+    n = e8.size
+    assert d8.numel() >= n, f"{what}: device buffer of {d8.numel()} B, expected {n} B"
+    for off in range(0, n, chunk):
+        m = min(chunk, n - off)
+        e = torch.from_numpy(e8[off:off + m]).to(DEV)
+        g = d8[off:off + m]
+        if not torch.equal(g, e):
+            bad = (g != e).nonzero().reshape(-1)
+            raise AssertionError(f"{what}: {bad.numel()} of {m} bytes differ in "
+                                 f"[{off}, {off + m}); first at byte {off + int(bad[0])}")
+        del e
+    return n
+
+
 def gather(t: torch.Tensor, idx: np.ndarray, E: int) -> np.ndarray:
     """Elements idx of device buffer t (E-byte items), to the host."""
     v = t.view(TDT[E])

@@ -15,6 +15,7 @@ if not torch.cuda.is_available():  # pragma: no cover
 
 from paper_2403_01876_amd import dv, swap_model  # noqa: E402
 from tests import gpu_util as G  # noqa: E402
+from tests import oracle_par as OP  # noqa: E402
 
 
 def pinned(nbytes: int, byte: int) -> torch.Tensor:
@@ -197,6 +198,7 @@ def test_swaps_replay_from_a_graph(oracle_lib, engine):
         assert G.host(back).tobytes() == exp_back.tobytes(), rep
 
 
+@pytest.mark.timeout(900)
 def test_opt66b_round_robin_swapping(oracle_lib):
     """Four microbatches through two device slots, two rounds.
 
@@ -204,9 +206,10 @@ def test_opt66b_round_robin_swapping(oracle_lib):
     slot; the step writes one token per layer (emulated by streaming in a
     generated increment) and packs that increment on the compute stream;
     after the step only the step's token is swapped out, while the next
-    microbatch is swapped in on another stream.  Device reference caches get
-    the same token writes; at the end every host mirror, swapped back in,
-    equals its reference.
+    microbatch is swapped in on another stream.  At the end every host
+    mirror equals the oracle's over every byte: the generator's prompt cache
+    copied to the mirror's layout, then each of the microbatch's step tokens
+    unpacked at its position.
     """
     w = synth.make_workload(2)
     L, H, D, B, S, E = w.layers, w.heads, w.head_dim, w.batch, w.max_seq, w.elem_bytes
@@ -216,29 +219,21 @@ def test_opt66b_round_robin_swapping(oracle_lib):
     hl = oracle.Layout(oracle.DENSE, L, H, D, B, seq_cap=S_host, elem_bytes=E)
     seeds = [synth.derived_seed(w.seed, 0x100 + x) for x in range(M)]
     slots = [G.dev_const(dl.storage_bytes(), 0) for _ in range(w.device_slots)]
-    refs = [G.dev_filled(dl.storage_bytes(), seeds[x]) for x in range(M)]
     hosts = [pinned(hl.storage_bytes(), 0) for _ in range(M)]
     ds = dv.Cache(dv.DV_DENSE, L, H, D, B, slots, max_seq=S)
-    dr = dv.Cache(dv.DV_DENSE, L, H, D, B, refs, max_seq=S)
     hh = dv.Cache(dv.DV_DENSE, L, H, D, B, [t.data_ptr() for t in hosts], max_seq=S_host,
                   mem=dv.DV_MEM_HOST_PINNED)
-    lens = [np.full(B, 1000, np.int32) for _ in range(M)]
+    prompt = np.full(B, 1000, np.int32)
+    lens = [prompt.copy() for _ in range(M)]
     zero = np.zeros(B, np.int32)
     compute, s_out, s_in = torch.cuda.current_stream(), torch.cuda.Stream(), torch.cuda.Stream()
 
-    # the prompt caches start on the host
+    # the prompt caches start on the host: each generated in slot 0, swapped out
     for x in range(M):
-        dv.dv_swap_out(dr, x, hh, x, 0, L, zero, lens[x], compute)
-    compute.synchronize()
-    # sampled check of one mirror against the oracle's copy map
-    rng = np.random.default_rng(2)
-    nel = oracle_lib.wire_elems(dl, 0, L, zero, lens[1])
-    widx = rng.integers(0, nel, size=1 << 16)
-    i_dev = oracle_lib.wire_to_storage(dl, 0, L, zero, lens[1], widx)
-    i_host = oracle_lib.wire_to_storage(hl, 0, L, zero, lens[1], widx)
-    got = hosts[1].numpy().view(np.uint16)[i_host]
-    exp = synth.bytes_at(seeds[1], i_dev.astype(np.uint64) * np.uint64(E), E).astype(np.uint16)
-    assert np.array_equal(got, exp)
+        synth.device_fill(slots[0].data_ptr(), dl.storage_bytes(), seeds[x],
+                          stream=compute.cuda_stream)
+        dv.dv_swap_out(ds, 0, hh, x, 0, L, zero, lens[x], compute)
+        compute.synchronize()
 
     inc_n = L * 2 * B * H * D * E
     assert inc_n == 4718592
@@ -253,6 +248,7 @@ def test_opt66b_round_robin_swapping(oracle_lib):
     dv.dv_swap_in(hh, 0, ds, 0, 0, L, zero, lens[0], s_in)
     swapped_in[0].record(s_in)
     steps = 2 * M
+    written = [[] for _ in range(M)]  # (position, token seed) of each step, per microbatch
     for k in range(steps):
         x, slot, nxt = k % M, k % 2, (k + 1) % 2
         # prefetch the next microbatch into the other slot once its previous
@@ -265,10 +261,9 @@ def test_opt66b_round_robin_swapping(oracle_lib):
         # the step itself on the compute stream
         compute.wait_event(swapped_in[slot])
         pos = lens[x]
-        synth.device_fill(tok.data_ptr(), inc_n, synth.derived_seed(w.seed, 0x200 + k),
-                          stream=compute.cuda_stream)
+        tok_seed = synth.derived_seed(w.seed, 0x200 + k)
+        synth.device_fill(tok.data_ptr(), inc_n, tok_seed, stream=compute.cuda_stream)
         dv.dv_stream_in(ds, slot, 0, L, pos, pos + 1, tok, inc_n, compute)
-        dv.dv_stream_in(dr, x, 0, L, pos, pos + 1, tok, inc_n, compute)
         dv.dv_stream_out_token(ds, slot, 0, L, pos, inc, inc_n, compute)
         done = torch.cuda.Event()
         done.record(compute)
@@ -276,16 +271,27 @@ def test_opt66b_round_robin_swapping(oracle_lib):
         s_out.wait_event(done)
         dv.dv_swap_out(ds, slot, hh, x, 0, L, pos, pos + 1, s_out)
         slot_free[slot].record(s_out)
+        written[x].append((pos.copy(), tok_seed))
         lens[x] = pos + 1
-        # the packed increment equals the token just written
+        # the packed increment is the generated token just written
         compute.synchronize()
-        assert torch.equal(inc, tok)
+        G.assert_same_bytes(inc, synth.fill_bytes(inc_n, tok_seed), f"increment of step {k}")
     torch.cuda.synchronize()
-    # every mirror swapped back in equals its reference on [0, len)
+    del slots, inc, tok
+    torch.cuda.empty_cache()
     for x in range(M):
-        dv.dv_swap_in(hh, x, ds, 0, 0, L, zero, lens[x], compute)
-        compute.synchronize()
-        G.assert_dense_ranges_equal(slots[0], refs[x], L, B, H, S, D, E, 0, L, zero, lens[x])
+        exp = np.zeros(hl.storage_bytes(), np.uint8)
+        gen = synth.fill_bytes_parallel(dl.storage_bytes(), seeds[x])
+        OP.copy_ranges(oracle_lib, dl, gen, hl, exp, 0, L, zero, prompt)
+        del gen
+        for pos, tok_seed in written[x]:
+            OP.unpack(oracle_lib, hl, exp, 0, L, pos, pos + 1,
+                      synth.fill_bytes(inc_n, tok_seed))
+        got = hosts[x].numpy()
+        if not np.array_equal(got, exp):
+            bad = np.flatnonzero(got != exp)
+            raise AssertionError(f"mirror {x}: {bad.size} bytes differ, first at {bad[0]}")
+        del exp
 
 
 @pytest.mark.parametrize("compute_kind", ["null", "own", "alternating"])
