@@ -48,8 +48,9 @@
 extern "C" {
 #endif
 
-/* 2: dv_cache gained block_owner (the optional owner-map workspace). */
-#define DV_API_VERSION 2
+/* 2: dv_cache gained block_owner (the optional owner-map workspace).
+ * 3: dv_stream_in_noalloc. */
+#define DV_API_VERSION 3
 
 /* The library is built with hidden visibility; only these calls export. */
 #define DV_API __attribute__((visibility("default")))
@@ -203,6 +204,33 @@ DV_API int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int3
  * DV_ERR_HIP. */
 DV_API int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
                  const int32_t* t1, const void* src, uint64_t src_bytes, void* stream);
+
+/* dv_stream_in for callers that cannot allocate and so can pass no owner-map
+ * workspace: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation.  Identical to dv_stream_in (same arguments,
+ * results, conditions for the pool-order scatter and errors), except that a
+ * paged receiver's owner map is built in a buffer of the library's own
+ * instead of dst->block_owner, which is ignored: a static device array of
+ * DV_NOALLOC_MAX_BLOCKS int32 entries (4 MiB), one per GPU, reserved when
+ * the library's code object is first loaded on that GPU and held until the
+ * process ends.  The call allocates nothing (no hipMalloc, no allocating
+ * library routine); its first call on a device looks the array's address up
+ * there once.  The current device's array is used, so `stream` must belong
+ * to the current device.  Paged receivers with more than
+ * DV_NOALLOC_MAX_BLOCKS blocks are refused with DV_ERR_UNSUPPORTED before
+ * anything is enqueued.  Every call that uses the array rebuilds the map in
+ * it (cleared by a kernel, then filled), so nothing carries over from the
+ * previous call; but all calls on one GPU share that GPU's array, so two
+ * calls whose work overlaps in time on one GPU (different streams, or
+ * different host threads) race on it and leave their pools undefined --
+ * order them on one stream or synchronise between them.  Dense and
+ * split-key receivers use no buffer and behave exactly as dv_stream_in.
+ * DV_OK, DV_ERR_INVALID, DV_ERR_RANGE, DV_ERR_SPACE, DV_ERR_UNSUPPORTED,
+ * DV_ERR_HIP. */
+#define DV_NOALLOC_MAX_BLOCKS (1 << 20)
+DV_API int dv_stream_in_noalloc(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1,
+                                const int32_t* t0, const int32_t* t1, const void* src,
+                                uint64_t src_bytes, void* stream);
 
 /* Debug check of a paged table over token ranges [t0[b], t1[b]) (t0 may be
  * NULL): writes to `counts` (device int32 [num_blocks], caller owned,

@@ -27,7 +27,8 @@ def _run(cmd):
 
 def build_libdv(out: str = LIBDV) -> str:
     srcs = [os.path.join(PKG, "csrc", f) for f in ("dv_kernels.hip", "dv_api.cpp",
-                                                    "dv_swapper.cpp", "dv_streamer.cpp")]
+                                                    "dv_swapper.cpp", "dv_streamer.cpp",
+                                                    "dv_noalloc.hip")]
     tmp = out + ".tmp"
     _run([HIPCC, *HIP_FLAGS, "-x", "hip", *srcs, "-o", tmp])
     os.replace(tmp, out)

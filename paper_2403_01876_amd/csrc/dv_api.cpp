@@ -615,11 +615,30 @@ int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
   return stream_out(src, mb, l0, l1, a.data(), e.data(), dst, dst_cap, out_bytes, stream);
 }
 
-int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
-                 const int32_t* t1, const void* src, uint64_t src_bytes, void* stream) {
+}  // extern "C"
+
+namespace dv {
+int noalloc_owner_map(int32_t** out);  // dv_noalloc.hip
+}  // namespace dv
+
+namespace {
+
+// dv_stream_in, and with `noalloc` dv_stream_in_noalloc: a paged receiver's
+// owner map then lives in the library's static per-device array instead of
+// the caller's workspace.
+int stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
+              const int32_t* t1, const void* src, uint64_t src_bytes, void* stream,
+              bool noalloc) {
+  dv_cache own;
+  if (noalloc && dst) {
+    own = *dst;
+    own.block_owner = nullptr;  // the caller's workspace, if any, is ignored
+    dst = &own;
+  }
   View v;
   int rc = view_of(dst, mb, &v);
   if (rc != DV_OK) return rc;
+  if (noalloc && v.kind == DV_PAGED && v.NB > DV_NOALLOC_MAX_BLOCKS) return DV_ERR_UNSUPPORTED;
   std::vector<int32_t> r0, rn;
   int64_t N = 0;
   rc = ranges_of(v, l0, l1, t0, t1, &r0, &rn, &N);
@@ -636,8 +655,27 @@ int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const 
     return DV_ERR_INVALID;
   rc = check_kind_supported(v);
   if (rc != DV_OK) return rc;
+  if (noalloc && v.kind == DV_PAGED) {
+    rc = dv::noalloc_owner_map(&v.owner);
+    if (rc != DV_OK) return rc;
+  }
   return run_stream(dv::kUnpack, v, l0, l1, r0, rn, N, const_cast<void*>(src),
                     static_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int32_t* t0,
+                 const int32_t* t1, const void* src, uint64_t src_bytes, void* stream) {
+  return stream_in(dst, mb, l0, l1, t0, t1, src, src_bytes, stream, false);
+}
+
+int dv_stream_in_noalloc(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1,
+                         const int32_t* t0, const int32_t* t1, const void* src,
+                         uint64_t src_bytes, void* stream) {
+  return stream_in(dst, mb, l0, l1, t0, t1, src, src_bytes, stream, true);
 }
 
 int dv_block_claims(const dv_cache* c, int32_t mb, const int32_t* t0, const int32_t* t1,

@@ -50,7 +50,7 @@ class dv_cache(ctypes.Structure):
     ]
 
 
-API_VERSION = 2  # DV_API_VERSION the dv_cache layout above matches
+API_VERSION = 3  # DV_API_VERSION the dv_cache layout and calls here match
 
 
 def _load():
@@ -71,6 +71,7 @@ def _load():
         "dv_stream_out_prompt": [P, i32, i32, i32, vp, vp, vp, u64, u64p, vp],
         "dv_stream_out_token": [P, i32, i32, i32, vp, vp, u64, u64p, vp],
         "dv_stream_in": [P, i32, i32, i32, vp, vp, vp, u64, vp],
+        "dv_stream_in_noalloc": [P, i32, i32, i32, vp, vp, vp, u64, vp],
         "dv_swap_out": [P, i32, P, i32, i32, i32, vp, vp, vp],
         "dv_swap_in": [P, i32, P, i32, i32, i32, vp, vp, vp],
         "dv_block_claims": [P, i32, vp, vp, vp, vp],
@@ -106,7 +107,8 @@ EXPORTS = ("dv_cache_bytes", "dv_packed_bytes", "dv_stream_out_prompt", "dv_stre
            "dv_swapper_create", "dv_swapper_prefetch", "dv_swapper_begin_step",
            "dv_swapper_end_step", "dv_swapper_sync", "dv_swapper_destroy",
            "dv_streamer_create", "dv_streamer_push", "dv_streamer_flush", "dv_streamer_destroy",
-           "dv_block_claims")
+           "dv_block_claims", "dv_stream_in_noalloc")
+NOALLOC_MAX_BLOCKS = 1 << 20  # DV_NOALLOC_MAX_BLOCKS
 
 
 def status_string(status: int) -> str:
@@ -234,6 +236,15 @@ def dv_stream_in(dst: Cache, mb: int, l0: int, l1: int, t0, t1, src, src_bytes: 
     a1, p1 = _i32(t1, dst.c.batch)
     rc = lib.dv_stream_in(dst.ref, mb, l0, l1, p0, p1, _addr(src), src_bytes, _stream(stream))
     return _check(rc, "dv_stream_in", check)
+
+
+def dv_stream_in_noalloc(dst: Cache, mb: int, l0: int, l1: int, t0, t1, src, src_bytes: int,
+                         stream=None, check: bool = True) -> int:
+    a0, p0 = _i32(t0, dst.c.batch)
+    a1, p1 = _i32(t1, dst.c.batch)
+    rc = lib.dv_stream_in_noalloc(dst.ref, mb, l0, l1, p0, p1, _addr(src), src_bytes,
+                                  _stream(stream))
+    return _check(rc, "dv_stream_in_noalloc", check)
 
 
 def dv_block_claims(cache: Cache, mb: int, t0, t1, counts, stream=None,

@@ -26,7 +26,7 @@ def test_library_exports_every_declared_function():
     lib = ctypes.CDLL(dv.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
-    assert dv.dv_api_version() == dv.API_VERSION == 2
+    assert dv.dv_api_version() == dv.API_VERSION == 3
 
 
 def test_status_strings():
@@ -138,6 +138,34 @@ def test_owner_workspace_rejections():
     rc, _ = dv.dv_stream_out_prompt(paged(FAKE + (1 << 36) + 2), 0, 0, L, None, t1, wire, need,
                                     check=False)
     assert rc == dv.DV_ERR_INVALID
+
+
+def test_noalloc_stream_in_limits():
+    """dv_stream_in_noalloc refuses a paged pool past its static owner map
+    (DV_NOALLOC_MAX_BLOCKS blocks) before anything else; at the limit the
+    call gets as far as the ordinary argument checks.  The workspace field
+    of the descriptor is ignored, misaligned or not."""
+    z, t1 = np.zeros(1, np.int32), np.ones(1, np.int32)
+
+    def pool(nb, owner=None):
+        return dv.Cache(dv.DV_PAGED, 1, 1, 64, 1, [FAKE], block_size=16, num_blocks=nb,
+                        max_blocks=4, block_tables=[FAKE + (1 << 36)], block_owners=[owner])
+
+    over = pool(dv.NOALLOC_MAX_BLOCKS + 1)
+    assert dv.dv_stream_in_noalloc(over, 0, 0, 1, z, t1, FAKE + (1 << 38), 1 << 20,
+                                   check=False) == dv.DV_ERR_UNSUPPORTED
+    at = pool(dv.NOALLOC_MAX_BLOCKS, owner=FAKE + (1 << 37) + 2)
+    assert dv.dv_stream_in_noalloc(at, 0, 0, 1, z, t1, None, 1 << 20,
+                                   check=False) == dv.DV_ERR_INVALID  # null source
+    assert dv.dv_stream_in_noalloc(at, 0, 0, 1, z, t1, FAKE + (1 << 38), 16,
+                                   check=False) == dv.DV_ERR_SPACE
+    # the same descriptor through dv_stream_in: the misaligned workspace counts
+    assert dv.dv_stream_in(at, 0, 0, 1, z, t1, FAKE + (1 << 38), 1 << 20,
+                           check=False) == dv.DV_ERR_INVALID
+    dense = dv.Cache(dv.DV_DENSE, 1, 1, 64, 1, [FAKE], max_seq=8)
+    assert dv.dv_stream_in_noalloc(dense, 0, 0, 1, z, np.array([9], np.int32),
+                                   FAKE + (1 << 38), 1 << 20,
+                                   check=False) == dv.DV_ERR_RANGE
 
 
 def test_block_table_must_not_overlap_what_a_call_writes():
@@ -408,7 +436,7 @@ def test_header_and_library_from_c(tmp_path):
     n, cache, rc, *rest = run.stdout.split()
     assert int(n) == 10 * 2 * 40 * 128 * 2 * (512 + 600 + 700 + 800 + 900 + 1000 + 1024)
     assert int(cache) == 10 * 2 * 8 * 40 * 2048 * 128 * 2
-    assert int(rc) == dv.DV_ERR_RANGE and rest[-1] == "2"
+    assert int(rc) == dv.DV_ERR_RANGE and rest[-1] == str(dv.API_VERSION)
 
 
 def test_descriptor_keeps_its_buffers_alive():
