@@ -1,29 +1,34 @@
 #!/usr/bin/env python3
 """KV-cache streaming benchmark on one MI355X.
 
-A step is one pass of the streaming hot path over the OPT-13B pipeline-stage
-workload (10 of 40 layers, 40 heads x 128, batch 8, capacity 2048, fp16,
-prompt lengths uniform 512..1024 from the seed):
+A step is one pass of the streaming hot path over the largest workload, the
+LLaMA-2-70B-shaped paged pool (20 of 80 layers, 8 KV heads x 128, block 16,
+32 sequences of U[128, 4096] tokens from the seed, fp16):
 
-  prompt stream-out (dense pack) -> prompt stream-in into a second cache
-  (dense unpack) -> 128 decode-step increments, each packed out of the
-  sender and streamed into the receiver.
+  paged gather of the prompt caches through table A (pack) -> scatter of the
+  contiguous buffer into a second pool through the freshly permuted table B
+  (unpack, in pool order through an owner-map workspace) -> 128 decode steps,
+  each tail-block increment packed out of pool A and streamed into pool B.
 
 Inputs are resident in HBM before timing starts.  The step's 258 calls are
-captured once into a HIP graph and the graph is replayed (the decode-step
-increments are launch-bound, 1.6 MB each); the same step issued call by call
-is timed too and reported as ``eager_ms_per_step`` (``--eager`` makes it the
-headline).  ``value`` is algorithmic bytes per step (every payload byte read
-once and written once: 2 x payload per call) over the step time, in GB/s.
-``roofline`` is the bulk pack kernel (the dense-run kernel of the prompt
-stream-out), its duration from HIP events around back-to-back launches on its
-stream, with a plain copy of the same bytes beside it (``copy_ceiling``).
-Further objects report the other kernels, the microbatch swap over the host
-link and the swap scheduler's protocol (OPT-66B stage), the paged
-gather/scatter (LLaMA-2-70B GQA), the full-cache replica and restore
-(BLOOM-176B shard), multi-token steps, streaming overlapped with emulated
-compute, ring recovery, buffered against per-region copies, and the oracle
-timed on the host cores.
+captured once into a HIP graph and the graph is replayed (the increments are
+launch-bound, 2.6 MB each); the same step issued call by call is timed too
+and reported as ``eager_ms_per_step`` (``--eager`` makes it the headline).
+``value`` is algorithmic bytes per step (every payload byte read once and
+written once: 2 x payload per call) over the step time, in GB/s.
+``roofline`` is the paged gather kernel, its duration from HIP events around
+back-to-back launches on its stream, with two ceilings beside it: a plain
+contiguous copy of the same bytes, and a copy of the whole pool block by
+block in the table's order (the gather's random block placement).
+``rooflines`` lists every bulk operation measured, per workload.  Further
+objects report the OPT-13B stage step (prompt and increments, with the dense
+pack kernel's roofline), the other kernels, the microbatch swap over the
+host link and the swap scheduler's protocol (OPT-66B stage), the full-cache
+replica and restore (BLOOM-176B shard), multi-token steps, streaming
+overlapped with emulated compute, ring recovery, buffered against
+per-region copies, and the oracle timed on the host cores (multi- and
+single-threaded, and compared over every byte with the GPU's gather and
+scatter).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--eager]
                        [--extras all|bulk|calib|swap|none] [--no-cpu-baseline]
@@ -247,6 +252,175 @@ def main_step_bench(args, torch, dv, synth):
         "checks": checks,
     }
     del sender, recv, wire, incs, graph
+    torch.cuda.empty_cache()
+    return w, res
+
+
+def block_order(w, table):
+    """For the paged pool of workload ``w``: the pool blocks of every (layer,
+    K|V) slab in the order the block table visits them (sequence by sequence,
+    logical block by logical block), as global block indices.  The workload's
+    tables use every pool block once, so this is a permutation of all the
+    pool's blocks."""
+    nb = w.num_blocks
+    per_slab = np.asarray(table, np.int64).reshape(-1)
+    per_slab = per_slab[(per_slab >= 0) & (per_slab < nb)]
+    assert per_slab.size == nb and np.unique(per_slab).size == nb
+    slabs = np.arange(2 * w.layers, dtype=np.int64)[:, None] * nb
+    return (slabs + per_slab[None, :]).reshape(-1).astype(np.int32)
+
+
+def back_to_back_ms(torch, stream, fn, n):
+    """Mean duration of ``fn`` from one event pair around ``n`` back-to-back
+    calls that follow a leading untimed one, so the queue never drains and
+    the mean is pure kernel time (an event pair per launch would add its own
+    packets)."""
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    fn()
+    a.record(stream)
+    for _ in range(n):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / n
+
+
+def paged_step_bench(args, torch, dv, synth):
+    """The step on the LLaMA-2-70B paged pool (20 of 80 layers, 8 KV heads x
+    128, block 16, 32 sequences of U[128, 4096] tokens): paged gather of the
+    prompt caches through table A into one contiguous buffer, scatter of that
+    buffer into a second pool through the freshly permuted table B (pool
+    order, through an owner-map workspace), then 128 decode steps whose
+    tail-block increments are packed out of pool A and streamed into pool B.
+    Replayed as one captured HIP graph (the default) or issued call by call
+    (--eager); both are timed.  Then the bulk kernels alone, back to back,
+    with the sequential copy ceiling and the block-order ceiling beside
+    them."""
+    from paper_2403_01876_amd import baseline
+    dev = torch.device("cuda:0")
+    w = synth.make_workload(4)
+    L, H, D, B = w.layers, w.heads, w.head_dim, w.batch
+    nb, bs, mbk = w.num_blocks, w.block_size, w.max_blocks
+    stream = torch.cuda.current_stream()
+    pool_bytes = w.pool_bytes()
+    pool_a = torch.empty(pool_bytes, dtype=torch.uint8, device=dev)
+    synth.device_fill(pool_a.data_ptr(), pool_bytes, w.data_seed, stream=stream.cuda_stream)
+    pool_b = torch.zeros(pool_bytes, dtype=torch.uint8, device=dev)
+    bta = torch.from_numpy(w.block_table_a).to(dev)
+    btb = torch.from_numpy(w.block_table_b).to(dev)
+    owners = torch.empty(nb * 4, dtype=torch.uint8, device=dev)
+    kw = dict(block_size=bs, num_blocks=nb, max_blocks=mbk)
+    ca = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool_a], block_tables=[bta], **kw)
+    cb = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool_b], block_tables=[btb], block_owners=[owners],
+                  **kw)
+    cb_table = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool_b], block_tables=[btb], **kw)
+    t0, t1 = w.prompt_ranges()
+    P = dv.dv_packed_bytes(ca, 0, L, t0, t1)
+    wire = torch.empty(P, dtype=torch.uint8, device=dev)
+    pos = [w.step_positions(i) for i in range(w.steps)]
+    ends = [p + 1 for p in pos]
+    I = dv.dv_packed_bytes(ca, 0, L, pos[0], ends[0])
+    inc = torch.empty(I, dtype=torch.uint8, device=dev)
+
+    def gather(st):
+        dv.dv_stream_out_prompt(ca, 0, 0, L, t0, t1, wire, P, st)
+
+    def scatter(st):
+        dv.dv_stream_in(cb, 0, 0, L, t0, t1, wire, P, st)
+
+    def step(st):
+        gather(st)
+        scatter(st)
+        for i in range(w.steps):
+            dv.dv_stream_out_token(ca, 0, 0, L, pos[i], inc, I, st)
+            dv.dv_stream_in(cb, 0, 0, L, pos[i], ends[i], inc, I, st)
+
+    def timed(fn, n):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(n):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    full = (t1 + w.steps).astype(np.int32)
+    M = dv.dv_packed_bytes(ca, 0, L, t0, full)
+
+    def pools_agree():
+        """The step's invariant, on the device: pool B gathers through table
+        B to the same bytes as pool A through table A over [0, len + 128)."""
+        ga = torch.empty(M, dtype=torch.uint8, device=dev)
+        gb = torch.empty(M, dtype=torch.uint8, device=dev)
+        dv.dv_stream_out_prompt(ca, 0, 0, L, t0, full, ga, M, stream)
+        dv.dv_stream_out_prompt(cb, 0, 0, L, t0, full, gb, M, stream)
+        torch.cuda.synchronize()
+        ok = bool(torch.equal(ga, gb))
+        del ga, gb
+        return ok
+
+    for _ in range(args.warmup):
+        step(stream)
+    eager_ms = timed(lambda: step(stream), args.steps)
+    log(f"paged step, eager: {eager_ms:.3f} ms/step")
+    checks = {"eager_pool_b_gathers_to_pool_a": pools_agree()}
+    eager_wire = wire.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            step(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        graph.replay()
+    graph_ms = timed(graph.replay, args.steps)
+    log(f"paged step, graph: {graph_ms:.3f} ms/step")
+    pool_b.zero_()
+    wire.zero_()
+    graph.replay()
+    torch.cuda.synchronize()
+    checks["graph_pool_b_gathers_to_pool_a"] = pools_agree()
+    checks["graph_wire_equals_eager_wire"] = bool(torch.equal(wire, eager_wire))
+    del eager_wire, graph
+    ms = eager_ms if args.eager else graph_ms
+
+    # the bulk kernels alone; at least 20 launches averaged (single launches
+    # vary by about 1 %)
+    nk = max(args.steps, 20)
+    kern = {
+        "gather": back_to_back_ms(torch, stream, lambda: gather(stream), nk),
+        "scatter_pool_order": back_to_back_ms(torch, stream, lambda: scatter(stream), nk),
+        "scatter_table_order": back_to_back_ms(
+            torch, stream, lambda: dv.dv_stream_in(cb_table, 0, 0, L, t0, t1, wire, P, stream),
+            nk),
+    }
+    # ceilings, on the gather's own buffers (placement in HBM moves these
+    # figures by several percent from one allocation to another): the first P
+    # bytes of pool A copied contiguously into the buffer (the pack kernels'
+    # copy ceiling), and the whole pool A copied into pool B block by block in
+    # table A's order, random block reads (the gather's placement) and random
+    # block writes (the table-order scatter's)
+    kern["plain_copy"] = back_to_back_ms(
+        torch, stream, lambda: baseline.plain_copy(wire, pool_a, P, stream), nk)
+    checks["plain_copy_equals_source"] = bool(torch.equal(wire, pool_a[:P]))
+    order = torch.from_numpy(block_order(w, w.block_table_a)).to(dev)
+    nblk = int(order.numel())
+    blk_bytes = H * bs * D * w.elem_bytes
+    assert nblk * blk_bytes == pool_bytes
+    for name, sc, src, dst in (("block_copy_random_reads", False, pool_a, pool_b),
+                               ("block_copy_random_writes", True, pool_a, pool_b)):
+        kern[name] = back_to_back_ms(
+            torch, stream,
+            lambda: baseline.block_copy(dst, src, order, nblk, blk_bytes, sc, stream), nk)
+    step_bytes = 2 * P * 2 + w.steps * 2 * I * 2
+    res = {"ms": ms, "eager_ms": eager_ms, "graph_ms": graph_ms, "P": P, "I": I,
+           "pool_bytes": pool_bytes, "num_blocks": nb, "step_bytes": step_bytes,
+           "value": step_bytes / (ms * 1e-3) / 1e9, "kern": kern, "checks": checks}
+    del pool_a, pool_b, wire, inc, order
     torch.cuda.empty_cache()
     return w, res
 
@@ -1051,54 +1225,121 @@ def copy_calibration(torch, nbytes=4 << 30):
     ms = t.mean_ms()
     del a, b
     torch.cuda.empty_cache()
-    return {"bytes": nbytes, "ms": round(ms, 4), "GBps_2x": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}
+    return {"bytes": nbytes, "ms": round(ms, 4),
+            "GBps_2x": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}
 
 
-def cpu_baseline():
-    """The oracle on the host cores: prompt stream-out and stream-in of the
-    OPT-13B stage (all 10 layers, 1.26 GB payload), no increments."""
+def cpu_baseline(torch, dv, synth, reps=3):
+    """The oracle on the host cores, on the headline workload (the LLaMA-2-70B
+    paged pool): paged gather through table A, then scatter of that buffer
+    into a zeroed pool through table B.
+
+    * Multi-threaded: all 20 layers, one oracle call per layer [l, l+1) on as
+      many host threads as the process's CPU affinity allows (layer ranges
+      concatenate, so the slabs are independent); the oracle's code is the
+      same.  This is ``value``.
+    * Single-threaded: layers [0, 2), one oracle call per operation.
+    Each is the median of ``reps`` runs, in the step's GB/s (2 x payload per
+    operation).  The multi-threaded run's gather buffer and pool are then
+    compared over every byte with one gather and one pool-order scatter of
+    the GPU on the same generated pool."""
     import oracle
-    import synth
+    from oracle import par
 
-    w = synth.make_workload(1)
-    lay = oracle.Layout(oracle.DENSE, w.layers, w.heads, w.head_dim, w.batch,
-                        seq_cap=w.max_seq, elem_bytes=2)
+    w = synth.make_workload(4)
     orc = oracle.get()
-    cache = synth.fill_bytes(lay.storage_bytes(), w.data_seed)
-    recv = np.zeros_like(cache)
-    recv[::4096] = 0  # touch the pages before timing
+    threads = par.host_threads()
+    la = oracle.Layout(oracle.PAGED, w.layers, w.heads, w.head_dim, w.batch,
+                       block_size=w.block_size, num_blocks=w.num_blocks,
+                       block_table=w.block_table_a)
+    lb = oracle.Layout(oracle.PAGED, w.layers, w.heads, w.head_dim, w.batch,
+                       block_size=w.block_size, num_blocks=w.num_blocks,
+                       block_table=w.block_table_b)
     t0, t1 = w.prompt_ranges()
-    n = orc.wire_elems(lay, 0, w.layers, t0, t1) * 2
-    wire = np.empty(n, np.uint8)
-    wire[::4096] = 0
-    a = time.perf_counter()
-    import ctypes
-    p0 = np.ascontiguousarray(t0, np.int32)
-    p1 = np.ascontiguousarray(t1, np.int32)
-    rc = orc.lib.dvo_pack(ctypes.byref(lay._c), cache.ctypes.data, 0, w.layers, p0.ctypes.data,
-                          p1.ctypes.data, wire.ctypes.data)
-    b = time.perf_counter()
-    rc |= orc.lib.dvo_unpack(ctypes.byref(lay._c), recv.ctypes.data, 0, w.layers,
-                             p0.ctypes.data, p1.ctypes.data, wire.ctypes.data)
-    c = time.perf_counter()
-    assert rc == 0
-    secs = c - a
-    del cache, recv, wire
+    pool = synth.fill_bytes_parallel(la.storage_bytes(), w.data_seed)
+    recv = np.zeros(lb.storage_bytes(), np.uint8)
+
+    def timed(fn):
+        a = time.perf_counter()
+        out = fn()
+        return time.perf_counter() - a, out
+
+    # multi-threaded, all layers
+    mt = []
+    wire = None
+    for _ in range(reps):
+        tg, wire = timed(lambda: par.pack(orc, la, pool, 0, w.layers, t0, t1, threads))
+        recv[:] = 0
+        ts, _ = timed(lambda: par.unpack(orc, lb, recv, 0, w.layers, t0, t1, wire, threads))
+        mt.append((tg, ts))
+    P = wire.nbytes
+    # single-threaded, layers [0, 2)
+    l1 = 2
+    st = []
+    for _ in range(reps):
+        part = np.empty(orc.wire_elems(la, 0, l1, t0, t1) * 2, np.uint8)
+        tg, _ = timed(lambda: orc.pack_into(la, pool, 0, l1, t0, t1, part))
+        scratch = np.zeros(lb.storage_bytes() // w.layers * l1, np.uint8)
+        lb2 = oracle.Layout(oracle.PAGED, l1, w.heads, w.head_dim, w.batch,
+                            block_size=w.block_size, num_blocks=w.num_blocks,
+                            block_table=w.block_table_b)
+        ts, _ = timed(lambda: orc.unpack(lb2, scratch, 0, l1, t0, t1, part))
+        st.append((tg, ts))
+    Pst = part.nbytes
+    del scratch, part
+    med = lambda xs: float(np.median(xs))  # noqa: E731
+    mt_s = med([g + x for g, x in mt])
+    st_s = med([g + x for g, x in st])
+
+    # the GPU on the same generated pool, compared over every byte
+    dev = torch.device("cuda:0")
+    s = torch.cuda.current_stream()
+    pa = torch.empty(la.storage_bytes(), dtype=torch.uint8, device=dev)
+    synth.device_fill(pa.data_ptr(), la.storage_bytes(), w.data_seed, stream=s.cuda_stream)
+    pb = torch.zeros(lb.storage_bytes(), dtype=torch.uint8, device=dev)
+    own = torch.empty(w.num_blocks * 4, dtype=torch.uint8, device=dev)
+    kw = dict(block_size=w.block_size, num_blocks=w.num_blocks, max_blocks=w.max_blocks)
+    ca = dv.Cache(dv.DV_PAGED, w.layers, w.heads, w.head_dim, w.batch, [pa],
+                  block_tables=[torch.from_numpy(w.block_table_a).to(dev)], **kw)
+    cb = dv.Cache(dv.DV_PAGED, w.layers, w.heads, w.head_dim, w.batch, [pb],
+                  block_tables=[torch.from_numpy(w.block_table_b).to(dev)], block_owners=[own],
+                  **kw)
+    gw = torch.empty(P, dtype=torch.uint8, device=dev)
+    dv.dv_stream_out_prompt(ca, 0, 0, w.layers, t0, t1, gw, P, s)
+    dv.dv_stream_in(cb, 0, 0, w.layers, t0, t1, gw, P, s)
+    torch.cuda.synchronize()
+    gw_h, pb_h = gw.cpu().numpy(), pb.cpu().numpy()
+    del pa, pb, gw, own, ca, cb
+    torch.cuda.empty_cache()
+    parity = {"gather_buffer_bytes": P,
+              "gather_buffer_equal": bool(np.array_equal(gw_h, wire)),
+              "scattered_pool_bytes": int(recv.nbytes),
+              "scattered_pool_equal": bool(np.array_equal(pb_h, recv))}
+    del gw_h, pb_h, wire, recv, pool
     return {
-        "value": round(2 * 2 * n / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-        "sample": (f"prompt stream-out + stream-in of the OPT-13B stage, all {w.layers} "
-                   f"layers, {n} B payload, no increments; single-threaded C oracle "
-                   f"({b - a:.2f} s out, {c - b:.2f} s in)"),
+        "value": round(2 * 2 * P / mt_s / 1e9, 3), "unit": "GB/s", "cores": threads,
+        "kind": "oracle",
+        "sample": (f"LLaMA-2-70B paged pool, all {w.layers} layers: gather through table A "
+                   f"({P} B) + scatter into a zeroed pool through table B; one oracle call "
+                   f"per layer on {threads} threads; median of {reps} "
+                   f"({med([g for g, _ in mt]):.2f} s gather, {med([x for _, x in mt]):.2f} s "
+                   f"scatter)"),
+        "single_thread": {
+            "value": round(2 * 2 * Pst / st_s / 1e9, 3), "unit": "GB/s", "cores": 1,
+            "sample": (f"the same, layers [0, {l1}) ({Pst} B), one call per operation; median "
+                       f"of {reps} ({med([g for g, _ in st]):.2f} s gather, "
+                       f"{med([x for _, x in st]):.2f} s scatter)")},
+        "parity_vs_gpu": parity,
         "host_cpu": cpu_model(),
-        "affinity_cores": len(os.sched_getaffinity(0)),
+        "affinity_cores": threads,
         "per_op": cpu_baseline_per_op(orc),
     }
 
 
 def cpu_baseline_per_op(orc):
-    """The oracle on the other operations the benchmark times, each on a
-    bounded sample of its workload (layer 0 of the stage, or one decode
-    step), in the same 2 x payload GB/s."""
+    """The oracle, single-threaded, on the other operations the benchmark
+    times, each on a bounded sample of its workload (layer 0 of the stage, or
+    one decode step), in the same 2 x payload GB/s."""
     import oracle
     import synth
 
@@ -1109,24 +1350,20 @@ def cpu_baseline_per_op(orc):
         fn()
         return round(2 * nbytes / (time.perf_counter() - a) / 1e9, 3)
 
-    # paged gather / scatter: LLaMA-2-70B pool, layer 0 of 20
-    w = synth.make_workload(4)
-    la = oracle.Layout(oracle.PAGED, 1, w.heads, w.head_dim, w.batch, block_size=w.block_size,
-                       num_blocks=w.num_blocks, block_table=w.block_table_a)
-    lb = oracle.Layout(oracle.PAGED, 1, w.heads, w.head_dim, w.batch, block_size=w.block_size,
-                       num_blocks=w.num_blocks, block_table=w.block_table_b)
-    pool = synth.fill_bytes(la.storage_bytes(), w.data_seed)
+    # OPT-13B stage prompt, all 10 layers, one call each way
+    w = synth.make_workload(1)
+    ld = oracle.Layout(oracle.DENSE, w.layers, w.heads, w.head_dim, w.batch, seq_cap=w.max_seq)
+    cache = synth.fill_bytes_parallel(ld.storage_bytes(), w.data_seed)
     t0, t1 = w.prompt_ranges()
     box = {}
-    g = rate(orc.wire_elems(la, 0, 1, t0, t1) * 2,
-             lambda: box.setdefault("wire", orc.pack(la, pool, 0, 1, t0, t1)))
-    recv = np.zeros(lb.storage_bytes(), np.uint8)
-    sc = rate(box["wire"].nbytes, lambda: orc.unpack(lb, recv, 0, 1, t0, t1, box["wire"]))
-    out["llama2-70b-paged"] = {"gather_GBps_2x": g, "scatter_GBps_2x": sc,
-                               "sample": f"layer 0 of {w.layers}, {box['wire'].nbytes} B payload"}
-    del pool, recv, box
+    po = rate(orc.wire_elems(ld, 0, w.layers, t0, t1) * 2,
+              lambda: box.setdefault("wire", orc.pack(ld, cache, 0, w.layers, t0, t1)))
+    recv = np.zeros_like(cache)
+    pi = rate(box["wire"].nbytes, lambda: orc.unpack(ld, recv, 0, w.layers, t0, t1, box["wire"]))
+    out["opt13b-stage prompt"] = {"pack_GBps_2x": po, "unpack_GBps_2x": pi,
+                                  "sample": f"all {w.layers} layers, {box['wire'].nbytes} B"}
+    del cache, recv, box
     # split key: OPT-13B stage, layer 0 of 10
-    w = synth.make_workload(1)
     lk = oracle.Layout(oracle.KSPLIT, 1, w.heads, w.head_dim, w.batch, seq_cap=w.max_seq)
     cache = synth.fill_bytes(lk.storage_bytes(), w.data_seed)
     t0, t1 = w.prompt_ranges()
@@ -1163,25 +1400,32 @@ def cpu_baseline_per_op(orc):
     return out
 
 
-def counted_traffic(which: str = "traffic_bytes_per_launch"):
-    """HBM bytes per launch of the bulk pack kernel (or, with
-    ``traffic_bytes_per_launch_unpack``, the unpack kernel) from the committed
-    counter summary, or None if the kernel sources changed since it was taken."""
+def counted_traffic(profile: str, key: str):
+    """HBM bytes per launch from the ``key`` line of the committed counter
+    summary ``profiles/<profile>``, or None if the kernel sources changed
+    since the counters were taken (the summary records their hash)."""
     import hashlib
     import re
-    path = os.path.join(ROOT, "profiles", "dense_runs_hbm_traffic_opt13b_stage.md")
+    path = os.path.join(ROOT, "profiles", profile)
     try:
         text = open(path).read()
     except OSError:
         return None
     m_sha = re.search(r"^kernel_source_sha256: ([0-9a-f]{64})$", text, re.M)
-    m_t = re.search(r"^%s: (\d+)$" % re.escape(which), text, re.M)
+    m_t = re.search(r"^%s: (\d+)$" % re.escape(key), text, re.M)
     if not (m_sha and m_t):
         return None
+    return int(m_t.group(1)) if kernel_source_sha256() == m_sha.group(1) else None
+
+
+def kernel_source_sha256() -> str:
+    """Hash of the streaming kernels' sources (the kernels and their launch
+    descriptors), recorded with each counter summary."""
+    import hashlib
     h = hashlib.sha256()
     for f in ("dv_kernels.hip", "dv_internal.h"):
         h.update(open(os.path.join(ROOT, "paper_2403_01876_amd", "csrc", f), "rb").read())
-    return int(m_t.group(1)) if h.hexdigest() == m_sha.group(1) else None
+    return h.hexdigest()
 
 
 def cpu_model():
@@ -1195,6 +1439,96 @@ def cpu_model():
 
 
 import numpy as np  # noqa: E402
+
+
+DENSE_TRAFFIC = "dense_runs_hbm_traffic_opt13b_stage.md"
+PAGED_TRAFFIC = "paged_kernel_hbm_traffic_llama2_70b_paged.md"
+
+
+def gbs2(nbytes, ms):
+    """Algorithmic GB/s of an operation moving ``nbytes`` of payload (each
+    byte read once and written once) in ``ms``."""
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def opt13b_step(args, torch, dv, synth):
+    """The OPT-13B stage step with its dense pack kernel's roofline and copy
+    ceiling."""
+    w, r = main_step_bench(args, torch, dv, synth)
+    pack_gbs, unpack_gbs, copy_gbs = (gbs2(r["P"], r[k]) for k in ("pack_ms", "unpack_ms",
+                                                                      "copy_ms"))
+    return {
+        "workload": ("opt13b-stage: 10 layers x 40 heads x 128 dims, batch 8, capacity 2048, "
+                     "fp16 dense [layer][K|V][batch][head][seq][dim], prompts U[512,1024] from "
+                     "seed 1; step = prompt stream-out + stream-in + 128 x (increment out + "
+                     "in)"),
+        "value": round(r["value"], 2), "unit": "GB/s", "ms_per_step": round(r["ms"], 4),
+        "eager_ms_per_step": round(r["eager_ms"], 4), "graph_ms_per_step": round(r["graph_ms"], 4),
+        "payload_prompt_bytes": r["P"], "payload_increment_bytes": r["I"],
+        "algorithmic_bytes_per_step": r["step_bytes"], "checks": r["checks"],
+        "roofline": {
+            "kernel": "dense_runs_kernel<pack> (prompt stream-out)", "bound": "hbm",
+            "achieved": round(pack_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(pack_gbs / HBM_PEAK_GBS, 4),
+            "traffic": counted_traffic(DENSE_TRAFFIC, "traffic_bytes_per_launch"),
+            "avg_ms": round(r["pack_ms"], 4), "bytes_per_launch": 2 * r["P"],
+            "copy_ceiling": {
+                "what": "plain contiguous 16-byte copy of the same P bytes in the pack "
+                        "kernel's launch shape (libdv_baseline dvb_plain_copy)",
+                "avg_ms": round(r["copy_ms"], 4), "GBps": round(copy_gbs, 1),
+                "frac": round(copy_gbs / HBM_PEAK_GBS, 4),
+                "kernel_vs_copy": round(pack_gbs / copy_gbs, 4)},
+        },
+        "dense_runs_kernel<unpack>": {
+            "avg_ms": round(r["unpack_ms"], 4), "GBps_2x": round(unpack_gbs, 1),
+            "frac_hbm": round(unpack_gbs / HBM_PEAK_GBS, 4),
+            "kernel_vs_copy": round(unpack_gbs / copy_gbs, 4),
+            "traffic": counted_traffic(DENSE_TRAFFIC, "traffic_bytes_per_launch_unpack")},
+    }
+
+
+def roofline_rows(out, paged):
+    """One row per (workload, bulk operation) measured in this run: the
+    kernel, its GB/s and its fraction of the roofline (HBM, or the host link
+    for swaps)."""
+    rows = []
+
+    def row(cfg, op, kernel, gbs, peak=HBM_PEAK_GBS, bound="hbm", cache="warm, back to back"):
+        rows.append({"config": cfg, "op": op, "kernel": kernel, "bound": bound,
+                     "GBps": round(gbs, 1), "peak": peak, "frac": round(gbs / peak, 4),
+                     "cache_state": cache})
+
+    k, P = paged["kern"], paged["P"]
+    row("llama2-70b-paged", "paged gather (table order)", "paged_kernel<pack>",
+        gbs2(P, k["gather"]))
+    row("llama2-70b-paged", "paged scatter, pool order (owner map included)",
+        "owner_clear/build + paged_kernel<unpack>", gbs2(P, k["scatter_pool_order"]))
+    row("llama2-70b-paged", "paged scatter, table order", "paged_kernel<unpack>",
+        gbs2(P, k["scatter_table_order"]))
+    step = out.get("opt13b_step")
+    if step:
+        row("opt13b-stage", "prompt stream-out", "dense_runs_kernel<pack>",
+            step["roofline"]["achieved"])
+        row("opt13b-stage", "prompt stream-in", "dense_runs_kernel<unpack>",
+            step["dense_runs_kernel<unpack>"]["GBps_2x"])
+    cold = "cold: 512 MB written between calls"
+    for name, res in out.get("bulk", {}).items():
+        for op in ("stream_out", "stream_in", "stream_in_table_order"):
+            if op in res:
+                row(name, op, "paged_kernel" if "paged" in name else
+                    ("ksplit_kernel + dense_runs_kernel" if "split" in name
+                     else "dense_runs_kernel"), res[op]["GBps_2x"], cache=cold)
+    sw = out.get("swap")
+    if sw:
+        for op in ("swap_out", "swap_in"):
+            row("opt66b-stage-swap", op, "hipMemcpy2DAsync (DMA)", sw[op]["GBps"],
+                peak=PCIE_PEAK_GBS, bound="host link", cache="n/a")
+    tiny = out.get("tiny")
+    if tiny:
+        rows.append({"config": "tiny-dense", "op": "prompt stream-out / stream-in",
+                     "kernel": "dense_runs_kernel", "bound": "latency",
+                     "frac": None, "note": tiny["note"]})
+    return rows
 
 
 def main():
@@ -1214,10 +1548,14 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     log(f"device: {torch.cuda.get_device_name(0)}")
-    w, r = main_step_bench(args, torch, dv, synth)
-    pack_gbs = 2 * r["P"] / (r["pack_ms"] * 1e-3) / 1e9
-    unpack_gbs = 2 * r["P"] / (r["unpack_ms"] * 1e-3) / 1e9
-    copy_gbs = 2 * r["P"] / (r["copy_ms"] * 1e-3) / 1e9
+    w, r = paged_step_bench(args, torch, dv, synth)
+    k, P = r["kern"], r["P"]
+    g_gbs = gbs2(P, k["gather"])
+    copy_gbs = gbs2(P, k["plain_copy"])
+    rr_gbs = gbs2(r["pool_bytes"], k["block_copy_random_reads"])
+    rw_gbs = gbs2(r["pool_bytes"], k["block_copy_random_writes"])
+    sp_gbs = gbs2(P, k["scatter_pool_order"])
+    st_gbs = gbs2(P, k["scatter_table_order"])
     out = {
         "metric": METRIC,
         "value": round(r["value"], 2),
@@ -1233,12 +1571,15 @@ def main():
         "data": "synthetic",
         "device": device_facts(torch),
         "config": {
-            "workload": ("opt13b-stage: 10 layers x 40 heads x 128 dims, batch 8, capacity "
-                         "2048, fp16 dense [layer][K|V][batch][head][seq][dim], prompts "
-                         "U[512,1024] from seed 1; step = prompt stream-out + stream-in + "
-                         "128 x (increment out + in)"),
-            "payload_prompt_bytes": r["P"],
+            "workload": (f"llama2-70b-paged: 20 of 80 layers x 8 KV heads x 128 dims, block 16 "
+                         f"tokens, 32 sequences U[128,4096] from seed 4, fp16 pool "
+                         f"[layer][K|V][block][head][slot][dim] of {r['num_blocks']} blocks, "
+                         f"tables A and B random permutations of it; step = paged gather "
+                         f"through table A + scatter through table B (pool order) + 128 x "
+                         f"(tail-block increment out of pool A + into pool B)"),
+            "payload_gather_bytes": P,
             "payload_increment_bytes": r["I"],
+            "pool_bytes": r["pool_bytes"],
             "algorithmic_bytes_per_step": r["step_bytes"],
             "step_issue": "eager" if args.eager else "hip graph replay",
             "eager_ms_per_step": round(r["eager_ms"], 4),
@@ -1246,31 +1587,48 @@ def main():
             "checks": r["checks"],
         },
         "roofline": {
-            "kernel": "dense_runs_kernel<pack> (prompt stream-out)",
+            "kernel": "paged_kernel<pack> (paged gather through table A)",
             "bound": "hbm",
-            "achieved": round(pack_gbs, 1),
+            "achieved": round(g_gbs, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": round(pack_gbs / HBM_PEAK_GBS, 4),
-            "traffic": counted_traffic(),
-            "avg_ms": round(r["pack_ms"], 4),
-            "bytes_per_launch": 2 * r["P"],
+            "frac": round(g_gbs / HBM_PEAK_GBS, 4),
+            "traffic": counted_traffic(PAGED_TRAFFIC, "traffic_bytes_per_launch"),
+            "avg_ms": round(k["gather"], 4),
+            "bytes_per_launch": 2 * P,
             "copy_ceiling": {
-                "what": "plain contiguous 16-byte copy of the same P bytes in the pack "
-                        "kernel's launch shape (libdv_baseline dvb_plain_copy)",
-                "avg_ms": round(r["copy_ms"], 4),
-                "GBps": round(copy_gbs, 1),
+                "what": "plain contiguous 16-byte copy of P bytes from pool A into the "
+                        "gather's buffer, in the dense kernels' launch shape (dvb_plain_copy)",
+                "avg_ms": round(k["plain_copy"], 4), "GBps": round(copy_gbs, 1),
                 "frac": round(copy_gbs / HBM_PEAK_GBS, 4),
-                "kernel_vs_copy": round(pack_gbs / copy_gbs, 4),
-            },
+                "kernel_vs_copy": round(g_gbs / copy_gbs, 4)},
+            "block_order_ceiling": {
+                "what": "plain copy of the whole pool block by block in table A's order, "
+                        "random 32 KB block reads and sequential writes, in the paged "
+                        "kernel's launch shape (dvb_block_copy): the gather's block "
+                        "placement without its ranges and head split",
+                "bytes": 2 * r["pool_bytes"],
+                "avg_ms": round(k["block_copy_random_reads"], 4), "GBps": round(rr_gbs, 1),
+                "frac": round(rr_gbs / HBM_PEAK_GBS, 4),
+                "kernel_vs_ceiling": round(g_gbs / rr_gbs, 4)},
         },
         "kernels": {
-            "dense_runs_kernel<unpack>": {"avg_ms": round(r["unpack_ms"], 4),
-                                          "GBps_2x": round(unpack_gbs, 1),
-                                          "frac_hbm": round(unpack_gbs / HBM_PEAK_GBS, 4),
-                                          "kernel_vs_copy": round(unpack_gbs / copy_gbs, 4),
-                                          "traffic": counted_traffic(
-                                              "traffic_bytes_per_launch_unpack")},
+            "paged scatter, pool order (owner map + paged_kernel<unpack>)": {
+                "avg_ms": round(k["scatter_pool_order"], 4), "GBps_2x": round(sp_gbs, 1),
+                "frac_hbm": round(sp_gbs / HBM_PEAK_GBS, 4),
+                "traffic": counted_traffic(PAGED_TRAFFIC,
+                                           "traffic_bytes_per_launch_scatter_pool_order")},
+            "paged scatter, table order (paged_kernel<unpack>)": {
+                "avg_ms": round(k["scatter_table_order"], 4), "GBps_2x": round(st_gbs, 1),
+                "frac_hbm": round(st_gbs / HBM_PEAK_GBS, 4),
+                "traffic": counted_traffic(PAGED_TRAFFIC,
+                                           "traffic_bytes_per_launch_scatter_table_order"),
+                "block_order_ceiling": {
+                    "what": "the same block copy with random block writes and sequential "
+                            "reads: the table-order scatter's placement",
+                    "avg_ms": round(k["block_copy_random_writes"], 4),
+                    "GBps": round(rw_gbs, 1), "frac": round(rw_gbs / HBM_PEAK_GBS, 4),
+                    "kernel_vs_ceiling": round(st_gbs / rw_gbs, 4)}},
         },
     }
     extras = "none" if args.no_extras else args.extras
@@ -1290,6 +1648,8 @@ def main():
             torch.cuda.synchronize()
             torch.cuda.empty_cache()
 
+    if extras != "none":
+        extra("opt13b_step", "OPT-13B stage step", lambda: opt13b_step(args, torch, dv, synth))
     if extras == "calib":
         extra("calibration_d2d_copy", "", lambda: copy_calibration(torch))
     if extras == "bulk":
@@ -1319,16 +1679,21 @@ def main():
         extra("buffered_vs_per_region", "buffered vs per-region copies",
               lambda: buffered_vs_per_region(torch, dv, synth))
         extra("calibration_d2d_copy", "copy calibration", lambda: copy_calibration(torch))
+    out["rooflines"] = roofline_rows(out, r)
     if not args.no_cpu_baseline:
-        extra("cpu_baseline", "cpu baseline (oracle)", cpu_baseline)
+        extra("cpu_baseline", "cpu baseline (oracle)", lambda: cpu_baseline(torch, dv, synth))
     if errors:
         out["errors"] = errors
     print(json.dumps(out), flush=True)
     failed = [k for k, v in r["checks"].items() if not v]
+    failed += [f"opt13b_step: {k}" for k, v in out.get("opt13b_step", {}).get("checks",
+                                                                            {}).items() if not v]
     for name, res in out.get("bulk", {}).items():
         failed += [f"{name}: {k}" for k, v in res.items() if k.startswith("check_") and not v]
+    par = out.get("cpu_baseline", {}).get("parity_vs_gpu", {})
+    failed += [f"cpu_baseline: {k}" for k, v in par.items() if k.endswith("_equal") and not v]
     if failed:
-        log("invariant checks failed, numbers invalid: " + ", ".join(failed))
+        log("checks failed, numbers invalid: " + ", ".join(failed))
         sys.exit(1)
 
 

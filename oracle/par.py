@@ -1,4 +1,6 @@
-"""The oracle run layer by layer on host threads, for full-size parity.
+"""The oracle run layer by layer on host threads (full-size parity tests and
+the benchmark's CPU-baseline leg).  TEST INFRASTRUCTURE ONLY, like the rest
+of this package.
 
 The oracle moves one element at a time on one thread; the full-size
 workloads stream up to 11 GB per call.  Layer ranges concatenate: the stream
@@ -11,16 +13,20 @@ buffers and hands them to it, and ctypes releases the GIL during each call.
 """
 from __future__ import annotations
 
+import os
 from concurrent.futures import ThreadPoolExecutor
 from typing import Optional
 
 import numpy as np
 
-import synth
+
+def host_threads() -> int:
+    """The process's CPU affinity count."""
+    return max(1, len(os.sched_getaffinity(0)))
 
 
 def _run(fn, items, threads: Optional[int]):
-    with ThreadPoolExecutor(threads or synth.host_threads()) as ex:
+    with ThreadPoolExecutor(threads or host_threads()) as ex:
         list(ex.map(fn, items))
 
 

@@ -3,7 +3,9 @@
 ``per_region_copy``: one copy call per contiguous region (the comparison
 baseline of the paper's evaluation, Sec. 5.1).  ``plain_copy``: a contiguous
 16-byte copy with the pack kernel's launch shape, the ceiling the streaming
-kernels are set against.  Used by the benchmark and its tests only.
+kernels are set against.  ``block_copy``: a copy of whole blocks in a block
+table's order, the ceiling of the paged kernels.  Used by the benchmark and
+its tests only.
 """
 from __future__ import annotations
 
@@ -30,6 +32,9 @@ def _load():
         lib.dvb_per_region_copy.restype = ctypes.c_int64
         lib.dvb_plain_copy.argtypes = [vp, vp, ctypes.c_uint64, vp]
         lib.dvb_plain_copy.restype = ctypes.c_int
+        lib.dvb_block_copy.argtypes = [vp, vp, vp, ctypes.c_uint32, ctypes.c_uint32,
+                                       ctypes.c_int, vp]
+        lib.dvb_block_copy.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -50,3 +55,13 @@ def plain_copy(dst, src, nbytes: int, stream=None) -> None:
     rc = _load().dvb_plain_copy(dv._addr(dst), dv._addr(src), nbytes, dv._stream(stream))
     if rc != dv.DV_OK:
         raise dv.DvError(int(rc), "dvb_plain_copy")
+
+
+def block_copy(dst, src, order, nblocks: int, block_bytes: int, scatter: bool = False,
+               stream=None) -> None:
+    """Block ``order[c]`` of ``src`` to block c of ``dst`` (or, with
+    ``scatter``, block c of ``src`` to block ``order[c]`` of ``dst``)."""
+    rc = _load().dvb_block_copy(dv._addr(dst), dv._addr(src), dv._addr(order), nblocks,
+                                block_bytes, 1 if scatter else 0, dv._stream(stream))
+    if rc != dv.DV_OK:
+        raise dv.DvError(int(rc), "dvb_block_copy")

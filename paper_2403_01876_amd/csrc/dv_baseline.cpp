@@ -11,6 +11,13 @@
 // against: a contiguous 16-byte copy with their per-lane shape (two
 // nontemporal units per lane, loads before stores, 256 lanes per workgroup)
 // and their XCD dealing, so the only difference left is the cache layout.
+//
+// dvb_block_copy is the ceiling of the paged kernels: a plain copy of whole
+// blocks, one side in the order a block table gives and the other
+// sequential, in the paged kernel's launch shape (8 KB per workgroup,
+// consecutive workgroups on consecutive pieces of one block, no XCD
+// dealing).  It has the paged gather's (or the table-order scatter's) random
+// block placement without the streamed ranges and the head split.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -53,9 +60,62 @@ __global__ void __launch_bounds__(kCopyThreads)
   }
 }
 
+// One workgroup per 8 KB piece; block c of the sequential side pairs with
+// block order[c] of the other side (skipped if outside [0, nblocks)).
+__global__ void __launch_bounds__(kCopyThreads)
+    block_copy_kernel(const u32x4* src, u32x4* dst, const int32_t* order, uint32_t nblocks,
+                      uint32_t pieces, int scatter) {
+  constexpr uint32_t kPiece = kCopyThreads * kCopyUnroll;  // units per workgroup
+  const uint32_t c = blockIdx.x / pieces, p = blockIdx.x - c * pieces;
+  const int32_t o = order[c];
+  if (o < 0 || (uint32_t)o >= nblocks) return;
+  const uint64_t seq = ((uint64_t)c * pieces + p) * kPiece;
+  const uint64_t rnd = ((uint64_t)o * pieces + p) * kPiece;
+  const u32x4* from = src + (scatter ? seq : rnd);
+  u32x4* to = dst + (scatter ? rnd : seq);
+  u32x4 v[kCopyUnroll];
+#pragma unroll
+  for (int k = 0; k < kCopyUnroll; ++k)
+    v[k] = __builtin_nontemporal_load(from + k * kCopyThreads + threadIdx.x);
+#pragma unroll
+  for (int k = 0; k < kCopyUnroll; ++k)
+    __builtin_nontemporal_store(v[k], to + k * kCopyThreads + threadIdx.x);
+}
+
 }  // namespace
 
 extern "C" {
+
+// Copies `nblocks` blocks of `block_bytes` (a multiple of 8192; addresses
+// 16-byte aligned, the two regions disjoint): with scatter == 0 block
+// order[c] of `src` to block c of `dst` (random reads), else block c of `src`
+// to block order[c] of `dst` (random writes).  `order` is a device int32
+// array [nblocks], a permutation of [0, nblocks) for the copy to be whole;
+// entries outside that range are skipped.  DV_OK, DV_ERR_INVALID,
+// DV_ERR_UNSUPPORTED (2^31 or more pieces of 8 KB), DV_ERR_HIP.
+DV_API int dvb_block_copy(void* dst, const void* src, const int32_t* order, uint32_t nblocks,
+                          uint32_t block_bytes, int scatter, void* stream) {
+  const uintptr_t d = reinterpret_cast<uintptr_t>(dst), s = reinterpret_cast<uintptr_t>(src);
+  const uint64_t piece = (uint64_t)kCopyThreads * kCopyUnroll * 16;
+  if (!dst || !src || !order || (d & 15u) || (s & 15u) ||
+      (reinterpret_cast<uintptr_t>(order) & 3u) || block_bytes == 0 || block_bytes % piece)
+    return DV_ERR_INVALID;
+  const uint64_t bytes = (uint64_t)nblocks * block_bytes;
+  if (d < s + bytes && s < d + bytes && bytes) return DV_ERR_INVALID;
+  if (nblocks == 0) return DV_OK;
+  const uint64_t grid = (uint64_t)nblocks * (block_bytes / piece);
+  if (grid >= (1ull << 31)) return DV_ERR_UNSUPPORTED;
+  const u32x4* from = static_cast<const u32x4*>(src);
+  u32x4* to = static_cast<u32x4*>(dst);
+  uint32_t nb = nblocks, pieces = (uint32_t)(block_bytes / piece);
+  int sc = scatter ? 1 : 0;
+  void* args[] = {&from, &to, &order, &nb, &pieces, &sc};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&block_copy_kernel), dim3((uint32_t)grid),
+                         dim3(kCopyThreads), args, 0, static_cast<hipStream_t>(stream)) ==
+                 hipSuccess
+             ? DV_OK
+             : DV_ERR_HIP;
+}
 
 // Copies `bytes` (a multiple of 16; both addresses 16-byte aligned, the
 // regions disjoint) from `src` to `dst` on `stream`.  DV_OK, DV_ERR_INVALID,

@@ -375,6 +375,25 @@ def test_plain_copy_baseline_rejections():
     assert lib.dvb_plain_copy(FAKE, FAKE + 16, 0, None) == dv.DV_OK  # nothing to copy
 
 
+def test_block_copy_baseline_rejections():
+    """The paged kernels' block-order ceiling checks its arguments first."""
+    from paper_2403_01876_amd import baseline
+    lib = baseline._load()
+    bad = dv.DV_ERR_INVALID
+    far, order = FAKE + (1 << 34), FAKE + (1 << 36)
+    for dst, src, o, nb, bb in ((FAKE + 8, far, order, 4, 8192),   # misaligned destination
+                                (FAKE, far + 4, order, 4, 8192),   # misaligned source
+                                (FAKE, far, order + 2, 4, 8192),   # misaligned order
+                                (FAKE, far, None, 4, 8192),        # no order
+                                (FAKE, far, order, 4, 4096),       # block not whole pieces
+                                (FAKE, far, order, 4, 0),
+                                (FAKE, FAKE + 8192, order, 4, 8192)):  # overlapping
+        assert lib.dvb_block_copy(dst, src, o, nb, bb, 0, None) == bad, (dst, src, o, nb, bb)
+    assert lib.dvb_block_copy(FAKE, far, order, 0, 8192, 1, None) == dv.DV_OK  # nothing
+    assert lib.dvb_block_copy(FAKE, FAKE + (1 << 45), order, 1 << 31, 8192, 0,
+                              None) == dv.DV_ERR_UNSUPPORTED  # 2^31 pieces
+
+
 def test_binding_fails_loudly_without_the_library(tmp_path):
     """No fallback: a copy of the package without libdv.so refuses to import."""
     import shutil

@@ -424,6 +424,30 @@ def test_plain_copy_baseline(units):
     assert bool((dst[n:] == 0x5C).all())
 
 
+@pytest.mark.parametrize("scatter", [False, True])
+@pytest.mark.parametrize("block_kb", [8, 32])
+def test_block_copy_baseline(scatter, block_kb):
+    """The paged kernels' ceiling copies whole blocks in a permutation's
+    order: checked against numpy's block permutation; an out-of-range order
+    entry skips its block (its destination keeps the sentinel)."""
+    from paper_2403_01876_amd import baseline
+    nb, bb = 37, block_kb * 1024
+    src_h = synth.fill_bytes(nb * bb, block_kb + 100 * scatter)
+    order = np.random.default_rng(block_kb).permutation(nb).astype(np.int32)
+    order[5] = nb  # skipped
+    dst = G.dev_const(nb * bb, 0x5C)
+    baseline.block_copy(dst, G.to_dev(src_h), G.to_dev(order), nb, bb, scatter, stream())
+    torch.cuda.synchronize()
+    s = src_h.reshape(nb, bb)
+    exp = np.full((nb, bb), 0x5C, np.uint8)
+    ok = order < nb
+    if scatter:
+        exp[order[ok]] = s[ok]
+    else:
+        exp[ok] = s[order[ok]]
+    assert G.host(dst).tobytes() == exp.tobytes()
+
+
 def test_binding_follows_torchs_current_stream(oracle_lib):
     """stream=None means torch's current stream: under torch.cuda.stream(s)
     the pack runs after the work already queued on s (here a long spin and

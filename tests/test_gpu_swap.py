@@ -15,7 +15,7 @@ if not torch.cuda.is_available():  # pragma: no cover
 
 from paper_2403_01876_amd import dv, swap_model  # noqa: E402
 from tests import gpu_util as G  # noqa: E402
-from tests import oracle_par as OP  # noqa: E402
+from oracle import par as OP  # noqa: E402
 
 
 def pinned(nbytes: int, byte: int) -> torch.Tensor:

@@ -4,7 +4,7 @@ benchmark times, compared with the oracle over every byte.
 Each GPU input is the seeded generator's device fill; the oracle reads the
 same generator's host fill (the two fills are independent implementations of
 one definition).  The oracle runs one layer per call on host threads
-(``tests/oracle_par.py``; layer ranges concatenate), and each GPU result --
+(``oracle/par.py``; layer ranges concatenate), and each GPU result --
 contiguous buffer, receiver cache or paged pool -- is compared with the
 oracle's whole result on the device.  Receivers start from a sentinel byte,
 so bytes a stream must leave alone are compared too.
@@ -23,7 +23,7 @@ if not torch.cuda.is_available():  # pragma: no cover
 
 from paper_2403_01876_amd import dv  # noqa: E402
 from tests import gpu_util as G  # noqa: E402
-from tests import oracle_par as OP  # noqa: E402
+from oracle import par as OP  # noqa: E402
 
 SENTINEL = 0xA5
 

@@ -1,4 +1,4 @@
-"""The layer-by-layer threaded oracle (``tests/oracle_par.py``) used by the
+"""The layer-by-layer threaded oracle (``oracle/par.py``) used by the
 full-size parity tests gives the same bytes as one oracle call over the whole
 layer range, for every layout, with more threads than layers and fewer."""
 import numpy as np
@@ -6,7 +6,7 @@ import pytest
 
 import oracle
 import synth
-from tests import oracle_par
+from oracle import par as oracle_par
 from tests.test_oracle_pins import dense_case, paged_case, rng
 
 
