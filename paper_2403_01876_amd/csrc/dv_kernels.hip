@@ -533,22 +533,22 @@ hipError_t launch_paged(int dir, const PagedArgs& a, uint32_t tiles_per_slab, ui
   return launch(fn, dim3(tiles_per_slab, nslabs), a, s);
 }
 
+// Workgroups of kThreads lanes covering n items (n up to INT32_MAX).
+static uint32_t groups_of(int32_t n) { return (uint32_t)(((int64_t)n + kThreads - 1) / kThreads); }
+
 hipError_t launch_owner_map(const OwnerArgs& a, hipStream_t s) {
-  const uint32_t clear = (uint32_t)((a.num_blocks + kThreads - 1) / kThreads);
-  hipError_t e = launch((const void*)&owner_clear_kernel, dim3(clear), a, s);
+  hipError_t e = launch((const void*)&owner_clear_kernel, dim3(groups_of(a.num_blocks)), a, s);
   if (e != hipSuccess) return e;
-  const uint32_t cols = (uint32_t)((a.max_blocks + kThreads - 1) / kThreads);
-  return launch((const void*)&owner_build_kernel, dim3(cols, a.nseq), a, s);
+  return launch((const void*)&owner_build_kernel, dim3(groups_of(a.max_blocks), a.nseq), a, s);
 }
 
 hipError_t launch_block_claims(const OwnerArgs& a, bool clear, hipStream_t s) {
   if (clear) {
-    const uint32_t n = (uint32_t)((a.num_blocks + kThreads - 1) / kThreads);
-    const hipError_t e = launch((const void*)&claims_clear_kernel, dim3(n), a, s);
+    const hipError_t e =
+        launch((const void*)&claims_clear_kernel, dim3(groups_of(a.num_blocks)), a, s);
     if (e != hipSuccess) return e;
   }
-  const uint32_t cols = (uint32_t)((a.max_blocks + kThreads - 1) / kThreads);
-  return launch((const void*)&claims_count_kernel, dim3(cols, a.nseq), a, s);
+  return launch((const void*)&claims_count_kernel, dim3(groups_of(a.max_blocks), a.nseq), a, s);
 }
 
 hipError_t launch_token(int dir, const TokenArgs& a, uint32_t units_per_slab, uint32_t nslabs,
