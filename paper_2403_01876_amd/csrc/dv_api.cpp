@@ -163,6 +163,81 @@ bool overlaps_table(const View& v, const void* p, uint64_t n) {
   return v.bt && overlaps(p, n, v.bt, (uint64_t)v.B * v.max_blocks * 4);
 }
 
+// Whether a paged stream-in with an owner-map workspace scatters in pool
+// order: at most kPoolSeqMax sequences (their ranges travel in the launch's
+// arguments), at least two thirds of the pool's blocks written, and every
+// count inside the kernels' 32-bit arithmetic.  Pool order launches a
+// workgroup for every block, and one that finds nothing to write still costs
+// its launch and owner lookup: on MI355X, for the LLaMA-2-70B pool, pool
+// order lost 5 % to table order with 47 % of the blocks written and 3 % with
+// 57 %, broke even near 63 % and won 3 % at 71 % and 6 % at 95 %.
+bool pool_order_applies(const View& v, const std::vector<int32_t>& t0,
+                        const std::vector<int32_t>& n, int64_t N) {
+  const int64_t ngrp = (v.H + dv::kPagedHeads - 1) / dv::kPagedHeads;
+  if (v.B > dv::kPoolSeqMax || N >= (1ll << 31) || v.NB * ngrp >= (1ll << 31) ||
+      v.B * v.max_blocks >= (1ll << 31))
+    return false;
+  int64_t tiles = 0;
+  for (int64_t b = 0; b < v.B; ++b)
+    if (n[b] > 0) tiles += ((t0[b] + n[b] + v.bs - 1) / v.bs - t0[b] / v.bs) * ngrp;
+  return 3 * tiles >= 2 * v.NB * ngrp;
+}
+
+// Paged stream-in in pool order for more than 64 sequences: the owner map
+// of the whole call (one clearing launch, one building launch per group of
+// 64 sequences), then one launch over every (slab, pool block, head pair).
+int pool_order_stream_in(const View& v, int32_t l0, int32_t l1, const std::vector<int32_t>& t0,
+                         const std::vector<int32_t>& n, int64_t N, void* wire, hipStream_t st) {
+  dv::OwnerArgs o;
+  memset(&o, 0, sizeof o);
+  o.owner = v.owner;
+  o.bt = v.bt;
+  o.block_size = (int32_t)v.bs;
+  o.num_blocks = (int32_t)v.NB;
+  o.max_blocks = (int32_t)v.max_blocks;
+  hipError_t e = dv::launch_owner_clear(o, st);
+  if (e != hipSuccess) return hip_fail(e, "owner map launch");
+  for (int64_t g0 = 0; g0 < v.B; g0 += kSeqPerLaunch) {
+    o.nseq = (int32_t)std::min<int64_t>(kSeqPerLaunch, v.B - g0);
+    o.b0 = (int32_t)g0;
+    memset(&o.r, 0, sizeof o.r);
+    bool any = false;
+    for (int i = 0; i < o.nseq; ++i) {
+      o.r.t0[i] = t0[g0 + i];
+      o.r.n[i] = n[g0 + i];
+      any = any || n[g0 + i] > 0;
+    }
+    if (!any) continue;
+    e = dv::launch_owner_build(o, st);
+    if (e != hipSuccess) return hip_fail(e, "owner map launch");
+  }
+  dv::PoolOrderArgs a;
+  memset(&a, 0, sizeof a);
+  a.pool = v.base;
+  a.wire = wire;
+  a.owner = v.owner;
+  a.s_slab = v.NB * v.H * v.bs * v.du;
+  a.s_blk = v.H * v.bs * v.du;
+  a.s_h = v.bs * v.du;
+  a.m = {2 * l0, 1, 0, 0, N * v.H * v.du};
+  a.du = (int32_t)v.du;
+  a.heads = (int32_t)v.H;
+  a.nseq = (int32_t)v.B;
+  a.max_blocks = (int32_t)v.max_blocks;
+  a.block_size = (int32_t)v.bs;
+  a.num_blocks = (int32_t)v.NB;
+  int64_t p = 0;
+  for (int64_t b = 0; b < v.B; ++b) {
+    a.t0[b] = t0[b];
+    a.n[b] = n[b];
+    a.p[b] = (int32_t)p;  // below 2^31: N is
+    p += n[b];
+  }
+  const int64_t ngrp = (v.H + dv::kPagedHeads - 1) / dv::kPagedHeads;
+  e = dv::launch_paged_pool_order(a, (uint32_t)(v.NB * ngrp), 2 * (uint32_t)(l1 - l0), st);
+  return hip_fail(e, "paged pool-order launch");
+}
+
 // Enqueue the pack (dir = kPack) or unpack of the validated ranges.  The wire
 // is at `wire`; per (layer, K|V) slab it holds N*H*du units.
 int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector<int32_t>& t0,
@@ -200,6 +275,12 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
       if (grid >= (1ll << 31)) return DV_ERR_UNSUPPORTED;
     }
   }
+
+  // Paged stream-in in pool order: up to 64 sequences through paged_kernel
+  // in the loop below, more through one launch over the whole call.
+  const bool pool_order = dir == dv::kUnpack && v.kind == DV_PAGED && !single && !small &&
+                          v.owner && pool_order_applies(v, t0, n, N);
+  if (pool_order && v.B > kSeqPerLaunch) return pool_order_stream_in(v, l0, l1, t0, n, N, wire, st);
 
   int64_t p_group = 0;  // tokens of all earlier launch groups
   for (int64_t g0 = 0; g0 < v.B; g0 += kSeqPerLaunch) {
@@ -343,17 +424,7 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
       int64_t tiles = 0;
       for (int i = 0; i < nseq; ++i)
         if (r.n[i] > 0) tiles += ((r.t0[i] + r.n[i] + v.bs - 1) / v.bs - r.t0[i] / v.bs) * ngrp;
-      // Scatter in pool order through the owner map when the caller gave a
-      // workspace, all sequences fit one launch and the call writes at least
-      // two thirds of the pool's blocks.  Pool order launches a workgroup for
-      // every block, and one that finds nothing to write still costs its
-      // launch and owner lookup: on MI355X, for the LLaMA-2-70B pool, pool
-      // order lost 5 % to table order with 47 % of the blocks written and 3 %
-      // with 57 %, broke even near 63 % and won 3 % at 71 % and 6 % at 95 %.
-      const bool pool_order = dir == dv::kUnpack && v.owner && v.B <= kSeqPerLaunch &&
-                              3 * tiles >= 2 * v.NB * ngrp && v.NB * ngrp < (1ll << 31) &&
-                              v.B * v.max_blocks < (1ll << 31);
-      if (pool_order) {
+      if (pool_order) {  // all sequences in this one group
         dv::OwnerArgs o;
         memset(&o, 0, sizeof o);
         o.owner = v.owner;
@@ -363,10 +434,11 @@ int run_stream(int dir, const View& v, int32_t l0, int32_t l1, const std::vector
         o.num_blocks = (int32_t)v.NB;
         o.max_blocks = (int32_t)v.max_blocks;
         o.r = r;
-        const hipError_t e = dv::launch_owner_map(o, st);
+        hipError_t e = dv::launch_owner_clear(o, st);
+        if (e == hipSuccess) e = dv::launch_owner_build(o, st);
         if (e != hipSuccess) return hip_fail(e, "owner map launch");
         a.owner = v.owner;
-        tiles = v.NB * ngrp;  // below 2^31 by the condition above
+        tiles = v.NB * ngrp;  // below 2^31: checked by pool_order_applies
       }
       const hipError_t e = dv::launch_paged(dir, a, (uint32_t)tiles, 2 * nl, st);
       if (e != hipSuccess) return hip_fail(e, "paged kernel launch");

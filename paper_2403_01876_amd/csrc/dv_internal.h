@@ -46,7 +46,8 @@ struct DenseRunArgs {
 
 // Paged blocks: one workgroup per (slab, block, head pair).  Blocks are
 // taken in table order -- (sequence, logical block) -- or, when `owner` is
-// set, in pool order through the owner map.
+// set, in pool order through the owner map (launches with all sequences in
+// one group, b0 = 0).
 struct PagedArgs {
   void* pool;
   void* wire;
@@ -61,16 +62,39 @@ struct PagedArgs {
   SeqRanges r;
 };
 
+// Sequences a pool-order stream-in covers in one launch: their ranges and
+// token prefixes travel in the arguments (3 KB).
+constexpr int kPoolSeqMax = 256;
+
+// Paged stream-in in pool order for calls of more than 64 sequences: one
+// workgroup per (slab, pool block, head pair) of the whole call; the owner
+// map names each block's (sequence, logical block), and the sequence's
+// range and exclusive token prefix (over the call, < 2^31) come from the
+// arrays below.
+struct PoolOrderArgs {
+  void* pool;
+  void* wire;             // the call's contiguous buffer
+  const int32_t* owner;   // [num_blocks] owner map
+  int64_t s_slab, s_blk, s_h;  // as PagedArgs
+  SlabMap m;
+  int32_t du, heads, nseq, max_blocks;
+  int32_t block_size, num_blocks, pad0, pad1;
+  int32_t t0[kPoolSeqMax];  // first token of each sequence's range
+  int32_t n[kPoolSeqMax];   // tokens in the range
+  int32_t p[kPoolSeqMax];   // tokens of all earlier sequences
+};
+static_assert(sizeof(PoolOrderArgs) <= 3584, "pool-order arguments stay well under 4 KB");
+
 // Owner map of a paged table over the streamed ranges: owner[blk] =
 // b * max_blocks + j for each entry (b, j) whose logical block j holds a
 // streamed token of sequence b and whose block blk is in [0, num_blocks);
-// -1 for every other block.  Only launches with all sequences in one group
-// (b0 = 0) use it.
+// -1 for every other block.  Built by one clearing launch and one launch
+// per group of up to 64 sequences, b0 being the group's first sequence.
 struct OwnerArgs {
   int32_t* owner;
   const int32_t* bt;
   int32_t nseq, block_size, num_blocks, max_blocks;
-  int32_t b0, pad;  // block claims: index of the launch's first sequence
+  int32_t b0, pad;  // index of the launch's first sequence
   SeqRanges r;
 };
 
@@ -151,8 +175,12 @@ hipError_t launch_dense_runs(int dir, const DenseRunArgs& a, uint32_t tiles_per_
                              uint32_t nslabs, hipStream_t s);
 hipError_t launch_paged(int dir, const PagedArgs& a, uint32_t tiles_per_slab, uint32_t nslabs,
                         hipStream_t s);
-// Clears the owner map and fills it from the table (two launches).
-hipError_t launch_owner_map(const OwnerArgs& a, hipStream_t s);
+hipError_t launch_paged_pool_order(const PoolOrderArgs& a, uint32_t tiles_per_slab,
+                                   uint32_t nslabs, hipStream_t s);
+// Sets every entry of the owner map to -1.
+hipError_t launch_owner_clear(const OwnerArgs& a, hipStream_t s);
+// Fills the owner map from the table for sequences [b0, b0 + nseq).
+hipError_t launch_owner_build(const OwnerArgs& a, hipStream_t s);
 // Counts, per pool block, the table entries over the ranges of sequences
 // [b0, b0 + nseq) that map to it, into `a.owner` (int32 counts), clearing
 // the counts first when `clear` is set.

@@ -178,7 +178,7 @@ def test_paged_gather_scatter(oracle_lib, seed):
 def test_paged_scatter_pool_order(oracle_lib, seed):
     """Scatter with an owner-map workspace: the pool equals the oracle's
     unpack whichever order the library picks; when the header's conditions
-    hold (some run longer than 256 16-byte units, at most 64 sequences, at
+    hold (some run longer than 256 16-byte units, at most 256 sequences, at
     least two thirds of the pool's blocks written) the workspace holds the owner
     map afterwards, otherwise it is untouched.  A second call with another
     table reuses the stale workspace."""
@@ -222,7 +222,7 @@ def test_paged_scatter_pool_order(oracle_lib, seed):
         du = D * E // 16
         # runs of at most 256 units per (sequence, head) take the short-run
         # kernel, which scatters in stream order
-        pool_order = (n > 0 and B <= 64 and (t1 - t0).max() > 1 and
+        pool_order = (n > 0 and B <= 256 and (t1 - t0).max() > 1 and
                       (t1 - t0).max() * du > 256 and 3 * blocks >= 2 * nb)
         w = G.host(ws)
         assert (w[nb * 4:] == 0x7E).all(), "wrote past the workspace"
@@ -231,6 +231,40 @@ def test_paged_scatter_pool_order(oracle_lib, seed):
                     G.owner_map_expected(bt_b, nb, bs, t0, t1)).all()
         elif call == 0:
             assert (w[: nb * 4] == 0x7E).all()
+
+
+@pytest.mark.parametrize("B", [130, 256, 257])
+def test_paged_scatter_pool_order_many_sequences(oracle_lib, B):
+    """Pool order over several launch groups: one owner map for the whole
+    call (sequence indices past 64 included) and one launch over the pool,
+    up to 256 sequences; 257 sequences scatter in table order and leave the
+    workspace untouched.  Against the oracle over the whole pool, with
+    sequences of every length including empty ones."""
+    r = np.random.default_rng(4000 + B)
+    L, H, D, E, bs = 2, 3, 128, 2, 16
+    lens = [int(x) for x in r.integers(0, 90, size=B)]
+    lens[5] = 0
+    maxb = max((n + bs - 1) // bs for n in lens) + 1
+    bt, nb = synth.make_paged_tables(B, lens, bs, maxb)
+    lay = oracle.Layout(oracle.PAGED, L, H, D, B, elem_bytes=E, block_size=bs, num_blocks=nb,
+                        block_table=bt)
+    t0 = np.zeros(B, np.int32)
+    t1 = np.array(lens, np.int32)
+    n = oracle_lib.wire_elems(lay, 0, L, t0, t1) * E
+    wire_h = synth.fill_bytes(n, 4100 + B)
+    recv = G.dev_const(lay.storage_bytes(), 0xA5)
+    ws = G.dev_const(nb * 4, 0x7E)
+    c = dv.Cache(dv.DV_PAGED, L, H, D, B, [recv], elem_bytes=E, block_size=bs, num_blocks=nb,
+                 max_blocks=maxb, block_tables=[G.to_dev(bt)], block_owners=[ws])
+    dv.dv_stream_in(c, 0, 0, L, t0, t1, G.to_dev(wire_h), n, stream())
+    torch.cuda.synchronize()
+    exp = np.full(lay.storage_bytes(), 0xA5, np.uint8)
+    oracle_lib.unpack(lay, exp, 0, L, t0, t1, wire_h)
+    assert G.host(recv).tobytes() == exp.tobytes()
+    if B <= 256:
+        assert (G.host(ws).view(np.int32) == G.owner_map_expected(bt, nb, bs, t0, t1)).all()
+    else:
+        assert (G.host(ws) == 0x7E).all()
 
 
 @pytest.mark.parametrize("seed", range(6))
