@@ -200,7 +200,8 @@ static void case_stream(hipStream_t st, int kind, int L, int H, int D, int B, in
 }
 
 /* Paged gather through a permuted table, scatter into another permutation
-   (table order, then pool order through the owner-map workspace). */
+   (table order, pool order through the owner-map workspace, and pool order
+   through the library's own map with dv_stream_in_noalloc). */
 static void case_paged(hipStream_t st) {
   enum { L = 2, H = 6, D = 128, B = 5, BS = 16, MAXB = 12 };
   const int32_t t0[B] = {0, 17, 0, 5, 40};
@@ -278,7 +279,11 @@ static void case_paged(hipStream_t st) {
   EXPECT(dvo_unpack(&ob, rexp, 0, L, t0, t1, exp) == DVO_OK, "oracle paged unpack");
   void* owner = NULL;
   HIPCHECK(hipMalloc(&owner, (size_t)nb * 4));
-  for (int order = 0; order < 2; ++order) {
+  static const char* const kScatter[3] = {
+      "paged scatter in table order against the oracle",
+      "paged scatter in pool order against the oracle",
+      "paged scatter without allocation (dv_stream_in_noalloc) against the oracle"};
+  for (int order = 0; order < 3; ++order) {
     uint8_t* sentinel = host_const(bytes, 0x3C);
     void* recv = to_device(sentinel, bytes);
     void* rbase[1] = {recv};
@@ -287,17 +292,18 @@ static void case_paged(hipStream_t st) {
     dv_cache r = c;
     r.mb_base = rbase;
     r.block_table = tab_b;
-    r.block_owner = order ? own : NULL;
-    EXPECT(dv_stream_in(&r, 0, 0, L, t0, t1, wire, need, st) == DV_OK, "paged scatter");
+    r.block_owner = order == 1 ? own : NULL;
+    const int rc = order == 2 ? dv_stream_in_noalloc(&r, 0, 0, L, t0, t1, wire, need, st)
+                              : dv_stream_in(&r, 0, 0, L, t0, t1, wire, need, st);
+    EXPECT(rc == DV_OK, "paged scatter");
     HIPCHECK(hipStreamSynchronize(st));
     uint8_t* rgot = to_host(recv, bytes);
-    same(rgot, rexp, bytes, order ? "paged scatter in pool order against the oracle"
-                                  : "paged scatter in table order against the oracle");
+    same(rgot, rexp, bytes, kScatter[order]);
     free(sentinel);
     free(rgot);
     HIPCHECK(hipFree(recv));
   }
-  printf("paged: %d pool blocks, %llu bytes gathered and scattered both ways, bit-exact\n", nb,
+  printf("paged: %d pool blocks, %llu bytes gathered and scattered three ways, bit-exact\n", nb,
          (unsigned long long)need);
   ++cases;
   free(host);

@@ -103,3 +103,69 @@ def test_noalloc_dense_receiver_is_stream_in():
                             wire, n)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("B", [6, 100])
+def test_noalloc_scatter_replayed_from_a_graph(B):
+    """The callers it is for capture it: a gather and a dv_stream_in_noalloc
+    scatter captured into a HIP graph and replayed three times, with eager
+    work and a fresh sentinel pool between replays; every replay against the
+    oracle.  100 sequences take the pool-order launch over the whole call
+    (more than 64 sequences), 6 the scan-based one."""
+    orc = oracle.get()
+    L, H, D, E, bs = 2, 4, 128, 2, 16
+    r = np.random.default_rng(B)
+    lens = [int(x) for x in r.integers(20, 120, size=B)]
+    maxb = max((n + bs - 1) // bs for n in lens)
+    bta, nb = synth.make_paged_tables(B + 1, lens, bs, maxb)
+    btb, nb2 = synth.make_paged_tables(B + 2, lens, bs, maxb)
+    assert nb == nb2
+    la = oracle.Layout(oracle.PAGED, L, H, D, B, elem_bytes=E, block_size=bs, num_blocks=nb,
+                       block_table=bta)
+    lb = oracle.Layout(oracle.PAGED, L, H, D, B, elem_bytes=E, block_size=bs, num_blocks=nb,
+                       block_table=btb)
+    gen_h = synth.fill_bytes(la.storage_bytes(), 300 + B)
+    pool_a = G.to_dev(gen_h)
+    pool_b = G.dev_const(lb.storage_bytes(), SENTINEL)
+    kw = dict(block_size=bs, num_blocks=nb, max_blocks=maxb)
+    ca = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool_a], block_tables=[G.to_dev(bta)], **kw)
+    cb = dv.Cache(dv.DV_PAGED, L, H, D, B, [pool_b], block_tables=[G.to_dev(btb)], **kw)
+    t0 = np.zeros(B, np.int32)
+    t1 = np.array(lens, np.int32)
+    n = dv.dv_packed_bytes(ca, 0, L, t0, t1)
+    wire = G.dev_const(n, 0)
+    exp_wire = orc.pack(la, gen_h, 0, L, t0, t1)
+    exp_pool = np.full(lb.storage_bytes(), SENTINEL, np.uint8)
+    orc.unpack(lb, exp_pool, 0, L, t0, t1, exp_wire)
+    # one eager call first: the library looks its buffer's address up once
+    assert dv.dv_stream_out_prompt(ca, 0, 0, L, t0, t1, wire, n) == n
+    assert dv.dv_stream_in_noalloc(cb, 0, 0, L, t0, t1, wire, n) == dv.DV_OK
+    torch.cuda.synchronize()
+    G.assert_same_bytes(pool_b, exp_pool, "eager noalloc scatter")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            cur = torch.cuda.current_stream()
+            dv.dv_stream_out_prompt(ca, 0, 0, L, t0, t1, wire, n, cur)
+            dv.dv_stream_in_noalloc(cb, 0, 0, L, t0, t1, wire, n, cur)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        pool_b.fill_(SENTINEL)
+        wire.fill_(rep + 1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        G.assert_same_bytes(wire, exp_wire, f"replay {rep}: gather")
+        G.assert_same_bytes(pool_b, exp_pool, f"replay {rep}: noalloc scatter")
+        # eager work between replays on the library's shared map: a smaller
+        # stream-in (still over two thirds of the blocks, so in pool order)
+        # that rebuilds the map for other ranges
+        part = (t1 * 9 // 10).astype(np.int32)
+        m = dv.dv_packed_bytes(cb, 0, L, t0, part)
+        scratch = G.dev_const(lb.storage_bytes(), 0)
+        cs = dv.Cache(dv.DV_PAGED, L, H, D, B, [scratch], block_tables=[G.to_dev(btb)], **kw)
+        dv.dv_stream_in_noalloc(cs, 0, 0, L, t0, part, wire[:m], m)
+        torch.cuda.synchronize()
+        del scratch
