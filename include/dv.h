@@ -65,7 +65,8 @@ typedef enum {
   DV_ERR_SPACE = -3,       /* destination capacity (or source size) below the stream size */
   DV_ERR_UNSUPPORTED = -4, /* well-formed but not handled: swap of a paged or split-key cache;
                               a split-key cache with more than 32 16-byte groups per token;
-                              extents past the kernels' 32-bit index arithmetic -- token
+                              extents past the kernels' 32-bit index arithmetic -- more
+                              than 2^24 layers, token
                               capacity (max_seq, or max_blocks*block_size) above 2^24,
                               head_dim*elem_bytes above 2^20 bytes, num_heads*head_dim*
                               elem_bytes above 2^24 bytes, capacity*head_dim*elem_bytes above

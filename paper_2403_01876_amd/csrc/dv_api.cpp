@@ -82,8 +82,9 @@ int layout_of(const dv_cache* c, View* v) {
   } else {
     return DV_ERR_INVALID;
   }
-  // Extents whose products the kernels take in 32-bit arithmetic.
-  if (v->cap > (1 << 24) || v->du > (1 << 16) || v->H * v->du > (1 << 20) ||
+  // Extents whose products the kernels take in 32-bit arithmetic (a launch's
+  // first slab index, 2 * layer + 1, among them).
+  if (v->L > (1 << 24) || v->cap > (1 << 24) || v->du > (1 << 16) || v->H * v->du > (1 << 20) ||
       v->cap * v->du > (1ll << 30))
     return DV_ERR_UNSUPPORTED;
   // The paged kernel flattens (head pair, unit) over two heads of one block:

@@ -150,8 +150,12 @@ int main(int argc, char** argv) {
     const int32_t* r0 = next() % 8 ? t0.data() : nullptr;
     const int32_t* r1 = next() % 16 ? t1.data() : nullptr;
     const int32_t* rp = next() % 16 ? pos.data() : nullptr;
-    const int32_t l0 = (int32_t)pick({0, 0, 1, -1, 2});
-    const int32_t l1 = (int32_t)pick({1, 2, 4, 0, -1, INT32_MAX});
+    int32_t l0 = (int32_t)pick({0, 0, 1, -1, 2});
+    int32_t l1 = (int32_t)pick({1, 2, 4, 0, -1, INT32_MAX});
+    if (next() % 8 == 0 && c.num_layers > 0) {  // the descriptor's last layer
+      l0 = c.num_layers - 1;
+      l1 = c.num_layers;
+    }
     const int32_t mb = (int32_t)pick({0, 0, 1, -1, 2, INT32_MAX});
     void* buf = address();
     const uint64_t cap = (uint64_t)pick({0, 16, 1 << 20, 1ll << 40, -1});

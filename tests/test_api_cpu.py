@@ -491,6 +491,10 @@ def test_extent_limits_at_and_past_the_boundary():
     def sized(c, t1):
         return dv.dv_packed_bytes(c, 0, 1, z1, np.array([t1], np.int32), check=False)
 
+    # 2^24 layers (a launch's first slab index, 2 * layer + 1, is an int32)
+    assert sized(dense(L=1 << 24, H=1, D=8, B=1, S=1), 1) == (0, 2 * 16)
+    assert sized(dense(L=(1 << 24) + 1, H=1, D=8, B=1, S=1), 1)[0] == U
+    assert dv.dv_cache_bytes(dense(L=(1 << 24) + 1, H=1, D=8, B=1, S=1), check=False)[0] == U
     # token capacity 2^24 (dense max_seq)
     assert sized(dense(L=1, H=1, D=8, B=1, S=1 << 24), 1 << 24) == (0, 2 * 16 << 24)
     assert sized(dense(L=1, H=1, D=8, B=1, S=(1 << 24) + 1), 1)[0] == U
@@ -532,8 +536,8 @@ def test_extent_limits_at_and_past_the_boundary():
     assert sized_b(pg((1 << 10) - 1)) == (0, 2 * 16 * ((1 << 10) - 1))
     assert sized_b(pg(1 << 10))[0] == U
     # products that would wrap 64 bits are refused, not wrapped
-    assert sized(dense(L=1 << 30, H=1 << 4, D=128, B=1, S=1 << 24), 1)[0] == U
-    assert dv.dv_cache_bytes(dense(L=1 << 30, H=1 << 16, D=128, B=1 << 30, S=1 << 24),
+    assert sized(dense(L=1 << 24, H=1 << 4, D=128, B=1, S=1 << 24), 1)[0] == U
+    assert dv.dv_cache_bytes(dense(L=1 << 24, H=1 << 16, D=128, B=1 << 30, S=1 << 24),
                              check=False)[0] == U
 
 
