@@ -1684,6 +1684,9 @@ def main():
         extra("cpu_baseline", "cpu baseline (oracle)", lambda: cpu_baseline(torch, dv, synth))
     if errors:
         out["errors"] = errors
+    # device memory the run held at its peak (every cache, pool and buffer is
+    # a torch allocation; pinned host mirrors are not device memory)
+    out["device"]["peak_allocated_bytes"] = int(torch.cuda.max_memory_allocated())
     print(json.dumps(out), flush=True)
     failed = [k for k, v in r["checks"].items() if not v]
     failed += [f"opt13b_step: {k}" for k, v in out.get("opt13b_step", {}).get("checks",
