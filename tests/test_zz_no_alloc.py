@@ -7,7 +7,8 @@ order, as the benchmark times it), the second a smaller pool whose map
 covers fewer blocks, so stale entries of the first call lie past its end.
 Both results are compared over every byte with the workspace call's and with
 the oracle's; the caller's workspace passed in the noalloc call's descriptor
-is left untouched.
+is left untouched.  Graph replays of the call are checked too, including a
+process whose very first call is made under capture.
 """
 import numpy as np
 import pytest
@@ -169,3 +170,19 @@ def test_noalloc_scatter_replayed_from_a_graph(B):
         dv.dv_stream_in_noalloc(cs, 0, 0, L, t0, part, wire[:m], m)
         torch.cuda.synchronize()
         del scratch
+
+
+def test_noalloc_first_call_under_graph_capture():
+    """In a process of its own, the first allocation-free call is made under
+    graph capture, so the library's one-time lookup of its buffer's address
+    happens while the stream is being captured; the replays still scatter
+    the oracle's bytes (tests/noalloc_capture_first.py)."""
+    import os
+    import subprocess
+    import sys
+
+    script = os.path.join(os.path.dirname(os.path.abspath(__file__)), "noalloc_capture_first.py")
+    r = subprocess.run([sys.executable, "-u", script], capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok"), \
+        r.stdout[-2000:] + r.stderr[-4000:]
