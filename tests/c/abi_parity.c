@@ -2,7 +2,8 @@
  * libdv.so and the HIP runtime only (no Python, no torch), streams caches
  * through every streaming entry point on its own hipStream_t and compares
  * each result byte for byte with the CPU oracle (test infrastructure,
- * linked here as a checker).  Inputs come from the seeded host generator.
+ * linked here to compute the expected bytes).  Inputs come from the seeded
+ * host generator.
  *
  * Cases: dense and split-key prompt streams (layer sub-range, ragged and
  * empty ranges, several tiles per run) into sentinel receivers; decode-step
