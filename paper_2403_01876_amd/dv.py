@@ -152,6 +152,12 @@ class Cache:
         """``block_owners``: optional per-microbatch int32 [num_blocks] device
         workspaces (None entries allowed) that let bulk paged stream-ins
         scatter in pool order."""
+        # The library reads block_table[mb] and block_owner[mb] for every
+        # microbatch index it accepts (below num_mb = len(bases)) and cannot
+        # see the arrays' lengths, so shorter arrays are refused here.
+        for name, arr in (("block_tables", block_tables), ("block_owners", block_owners)):
+            if arr is not None and len(arr) != len(bases):
+                raise ValueError(f"{name} has {len(arr)} entries, bases has {len(bases)}")
         # Tensors and arrays given here stay referenced for the descriptor's
         # life, so a temporary cannot be freed while its address is in use.
         self._keep = [x for x in list(bases) + list(block_tables or []) +

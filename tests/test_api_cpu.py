@@ -541,6 +541,22 @@ def test_extent_limits_at_and_past_the_boundary():
                              check=False)[0] == U
 
 
+def test_binding_refuses_per_microbatch_arrays_of_another_length():
+    """The library reads block_table[mb] and block_owner[mb] for every
+    microbatch index below num_mb = len(bases); the binding refuses table
+    and owner arrays whose length differs from the bases'."""
+    kw = dict(block_size=16, num_blocks=4, max_blocks=2)
+    with pytest.raises(ValueError):
+        dv.Cache(dv.DV_PAGED, 1, 1, 8, 1, [FAKE, FAKE + (1 << 30)], block_tables=[FAKE], **kw)
+    with pytest.raises(ValueError):
+        dv.Cache(dv.DV_PAGED, 1, 1, 8, 1, [FAKE], block_tables=[FAKE],
+                 block_owners=[FAKE, FAKE], **kw)
+    c = dv.Cache(dv.DV_PAGED, 1, 1, 8, 1, [FAKE, FAKE + (1 << 30)],
+                 block_tables=[FAKE + (1 << 40), FAKE + (1 << 41)], block_owners=[None, None],
+                 **kw)
+    assert c.c.num_mb == 2
+
+
 def test_binding_refuses_range_arrays_shorter_than_the_batch():
     """The library reads one range entry per sequence and cannot see an
     array's length: the binding refuses a short one before the call."""
