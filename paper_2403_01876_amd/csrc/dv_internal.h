@@ -208,4 +208,12 @@ constexpr int kDenseTile = kThreads * kDenseUnroll;
 constexpr int kPagedHeads = 2;
 constexpr int kPagedUnroll = 2;
 
+// Pool-order scatters deal their (tile, slab) grid to the 8 XCDs in chunks
+// of this many consecutive tiles (8 pool blocks of one slab at 8 heads; 256
+// KB for the LLaMA-2-70B pool).  Measured on MI355X on that pool against the
+// hardware's round-robin dealing, contiguous eighths and chunks of 8, 16, 48
+// and 64 tiles; table-order kernels keep the round-robin order, which was
+// fastest for them.
+constexpr int kPoolChunk = 32;
+
 }  // namespace dv
