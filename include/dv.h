@@ -219,7 +219,9 @@ DV_API int dv_stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1,
  * process ends.  The call allocates nothing (no hipMalloc, no allocating
  * library routine); its first call on a device looks the array's address up
  * there once.  The current device's array is used, so `stream` must belong
- * to the current device.  Paged receivers with more than
+ * to the current device; a paged receiver's call on a stream of another
+ * device is refused with DV_ERR_INVALID before anything is enqueued.  Paged
+ * receivers with more than
  * DV_NOALLOC_MAX_BLOCKS blocks are refused with DV_ERR_UNSUPPORTED before
  * anything is enqueued.  Every call that uses the array rebuilds the map in
  * it (cleared by a kernel, then filled), so nothing carries over from the

@@ -694,7 +694,7 @@ int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int32_t l1,
 }  // extern "C"
 
 namespace dv {
-int noalloc_owner_map(int32_t** out);  // dv_noalloc.hip
+int noalloc_owner_map(hipStream_t stream, int32_t** out);  // dv_noalloc.hip
 }  // namespace dv
 
 namespace {
@@ -732,7 +732,7 @@ int stream_in(const dv_cache* dst, int32_t mb, int32_t l0, int32_t l1, const int
   rc = check_kind_supported(v);
   if (rc != DV_OK) return rc;
   if (noalloc && v.kind == DV_PAGED) {
-    rc = dv::noalloc_owner_map(&v.owner);
+    rc = dv::noalloc_owner_map(static_cast<hipStream_t>(stream), &v.owner);
     if (rc != DV_OK) return rc;
   }
   return run_stream(dv::kUnpack, v, l0, l1, r0, rn, N, const_cast<void*>(src),

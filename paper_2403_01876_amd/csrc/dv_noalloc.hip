@@ -24,11 +24,18 @@ int32_t* g_addr[kMaxDevices];  // device address of `scratch` per device, once l
 namespace dv {
 
 // The current device's copy of the array: DV_OK and its address, DV_ERR_HIP
-// if the runtime cannot name the device or the symbol, DV_ERR_UNSUPPORTED for
-// a device index past the table above.
-int noalloc_owner_map(int32_t** out) {
+// if the runtime cannot name the device or the symbol, DV_ERR_INVALID when
+// `stream` (not the null stream) belongs to another device, whose kernels
+// would then reach this device's copy, DV_ERR_UNSUPPORTED for a device index
+// past the table above.
+int noalloc_owner_map(hipStream_t stream, int32_t** out) {
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) return DV_ERR_HIP;
+  if (stream) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(stream, &sdev) != hipSuccess) return DV_ERR_HIP;
+    if (sdev != dev) return DV_ERR_INVALID;
+  }
   if (dev < 0 || dev >= kMaxDevices) return DV_ERR_UNSUPPORTED;
   std::lock_guard<std::mutex> lock(g_mu);
   if (!g_addr[dev]) {
