@@ -192,14 +192,14 @@ DV_API int dv_stream_out_token(const dv_cache* src, int32_t mb, int32_t l0, int3
  * sequence's run per head is longer than 4 KB (shorter runs go through a
  * kernel that moves one 16-byte unit per lane in stream order), the call
  * has at most 256 sequences and fewer than 2^31 tokens, and it writes at
- * least two thirds of the pool's blocks, the library first rebuilds in the
+ * least five ninths of the pool's blocks, the library first rebuilds in the
  * workspace the inverse of the table over the streamed ranges (pool block
  * -> sequence * max_blocks + logical block, -1 for blocks not written) and
  * then writes the pool in physical block order in one launch, so the
  * writes are sequential instead of scattered
- * by the table (measured on MI355X: 70 % -> 74 % of HBM peak for the
- * LLaMA-2-70B stage's pool; below two thirds of the blocks, the workgroups
- * that find no block to write cost more than that gains).  The bytes
+ * by the table (measured on MI355X: 69 % -> 75 % of HBM peak for the
+ * LLaMA-2-70B stage's pool; below about five ninths of the blocks, the
+ * workgroups that find no block to write cost more than that gains).  The bytes
  * written are the same either way.  The workspace must not overlap the
  * cache or `src` (DV_ERR_INVALID); its contents are scratch between calls,
  * and calls that scatter into the same microbatch must not overlap in time.

@@ -166,12 +166,13 @@ bool overlaps_table(const View& v, const void* p, uint64_t n) {
 
 // Whether a paged stream-in with an owner-map workspace scatters in pool
 // order: at most kPoolSeqMax sequences (their ranges travel in the launch's
-// arguments), at least two thirds of the pool's blocks written, and every
+// arguments), at least five ninths of the pool's blocks written, and every
 // count inside the kernels' 32-bit arithmetic.  Pool order launches a
 // workgroup for every block, and one that finds nothing to write still costs
 // its launch and owner lookup: on MI355X, for the LLaMA-2-70B pool, pool
-// order lost 5 % to table order with 47 % of the blocks written and 3 % with
-// 57 %, broke even near 63 % and won 3 % at 71 % and 6 % at 95 %.
+// order lost 4 % to table order with 47 % of the blocks written and 1 % with
+// 52 %, broke even near 54 % and won 1.5 % at 57 %, 3 % at 62 % and 7 % at
+// 95 %.
 bool pool_order_applies(const View& v, const std::vector<int32_t>& t0,
                         const std::vector<int32_t>& n, int64_t N) {
   const int64_t ngrp = (v.H + dv::kPagedHeads - 1) / dv::kPagedHeads;
@@ -181,7 +182,7 @@ bool pool_order_applies(const View& v, const std::vector<int32_t>& t0,
   int64_t tiles = 0;
   for (int64_t b = 0; b < v.B; ++b)
     if (n[b] > 0) tiles += ((t0[b] + n[b] + v.bs - 1) / v.bs - t0[b] / v.bs) * ngrp;
-  return 3 * tiles >= 2 * v.NB * ngrp;
+  return 9 * tiles >= 5 * v.NB * ngrp;
 }
 
 // Paged stream-in in pool order for more than 64 sequences: the owner map

@@ -161,7 +161,7 @@ def test_noalloc_scatter_replayed_from_a_graph(B):
         G.assert_same_bytes(wire, exp_wire, f"replay {rep}: gather")
         G.assert_same_bytes(pool_b, exp_pool, f"replay {rep}: noalloc scatter")
         # eager work between replays on the library's shared map: a smaller
-        # stream-in (still over two thirds of the blocks, so in pool order)
+        # stream-in (still over five ninths of the blocks, so in pool order)
         # that rebuilds the map for other ranges
         part = (t1 * 9 // 10).astype(np.int32)
         m = dv.dv_packed_bytes(cb, 0, L, t0, part)
