@@ -233,6 +233,36 @@ def test_paged_scatter_pool_order(oracle_lib, seed):
             assert (w[: nb * 4] == 0x7E).all()
 
 
+@pytest.mark.parametrize("written", [4, 5])
+def test_paged_scatter_pool_order_threshold(oracle_lib, written):
+    """The five-ninths rule at its boundary: a pool of 9 blocks with an
+    owner-map workspace, one sequence streaming 5 blocks (5/9: pool order,
+    the workspace holds the table's inverse) or 4 blocks (table order, the
+    workspace untouched).  The pool equals the oracle's unpack either way."""
+    L, H, D, B, E, bs, nb, maxb = 2, 2, 128, 1, 2, 16, 9, 9
+    r = np.random.default_rng(77 + written)
+    bt = r.permutation(nb).astype(np.int32).reshape(1, maxb)
+    lay = oracle.Layout(oracle.PAGED, L, H, D, B, elem_bytes=E, block_size=bs, num_blocks=nb,
+                        block_table=bt)
+    t0 = np.zeros(B, np.int32)
+    t1 = np.array([written * bs], np.int32)  # runs of 1024-1280 16-byte units: tiled kernels
+    n = oracle_lib.wire_elems(lay, 0, L, t0, t1) * E
+    wire_h = synth.fill_bytes(n, 500 + written)
+    recv = G.dev_const(lay.storage_bytes(), 0xA5)
+    ws = G.dev_const(nb * 4, 0x7E)
+    c = dv.Cache(dv.DV_PAGED, L, H, D, B, [recv], elem_bytes=E, block_size=bs, num_blocks=nb,
+                 max_blocks=maxb, block_tables=[G.to_dev(bt)], block_owners=[ws])
+    dv.dv_stream_in(c, 0, 0, L, t0, t1, G.to_dev(wire_h), n, stream())
+    torch.cuda.synchronize()
+    exp = np.full(lay.storage_bytes(), 0xA5, np.uint8)
+    oracle_lib.unpack(lay, exp, 0, L, t0, t1, wire_h)
+    assert G.host(recv).tobytes() == exp.tobytes()
+    if 9 * written >= 5 * nb:
+        assert (G.host(ws).view(np.int32) == G.owner_map_expected(bt, nb, bs, t0, t1)).all()
+    else:
+        assert (G.host(ws) == 0x7E).all()
+
+
 @pytest.mark.parametrize("B", [130, 256, 257])
 def test_paged_scatter_pool_order_many_sequences(oracle_lib, B):
     """Pool order over several launch groups: one owner map for the whole
